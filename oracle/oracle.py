@@ -1,0 +1,108 @@
+"""ctypes front end of the C fp64 oracle (``csr_oracle.c``) plus its build step.
+
+Test infrastructure only (see ``oracle/__init__.py``).  Each function names the
+passage of the paper it follows; the arithmetic lives in ``csr_oracle.c``.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import subprocess
+
+import numpy as np
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+SRC = os.path.join(HERE, "csr_oracle.c")
+LIB = os.path.join(HERE, "liboracle.so")
+
+F32, BF16 = 0, 1
+
+_lib = None
+
+
+def build() -> str:
+    """Compile the oracle with gcc (plain C, OpenMP)."""
+    cmd = ["gcc", "-O2", "-fopenmp", "-fPIC", "-shared", "-std=c11", SRC, "-o", LIB + ".tmp", "-lm"]
+    subprocess.run(cmd, check=True)
+    os.replace(LIB + ".tmp", LIB)
+    return LIB
+
+
+def _load():
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB) or os.path.getmtime(LIB) < os.path.getmtime(SRC):
+            build()
+        lib = ctypes.CDLL(LIB)
+        p, i, d = ctypes.c_void_p, ctypes.c_int, ctypes.c_double
+        lib.csr_oracle_attention.argtypes = [i, i, i, i, i, d, i, p, p, p, p, p, p, i, p, p, i, p, p, p, p, i]
+        lib.csr_oracle_attention.restype = i
+        lib.csr_oracle_kv_append.argtypes = [i, i, i, i, i, p, p, p, p, p, i, p, p]
+        lib.csr_oracle_kv_append.restype = i
+        _lib = lib
+    return _lib
+
+
+def _ptr(a):
+    return None if a is None else a.ctypes.data_as(ctypes.c_void_p)
+
+
+def _i32(a):
+    return None if a is None else np.ascontiguousarray(a, dtype=np.int32)
+
+
+def default_threads() -> int:
+    return len(os.sched_getaffinity(0))
+
+
+def attention(dtype, q, k_new, v_new, k_pool, v_pool, block_table, bt_stride, cu_seqlens_q,
+              cache_len, rows, num_q_heads, num_kv_heads, head_dim, page_size, scale=None,
+              nthreads=None):
+    """Extend attention for the query tokens in ``rows`` (all heads).
+
+    Paper Sec. II, eq. (causal_attention_1)-(causal_attention_3) over the
+    cached concatenation of eq. (K_cache)-(V_cache); prefix length L_b = i* - 1
+    (eq. (csr_i_star)).  ``cache_len=None`` is the L_b = 0 full re-prefill
+    (warm-up of Algorithm 1).  Arrays: bf16 as uint16 bit patterns, fp32 as
+    float32.  Returns ``(out [R,Hq,d] f64, lse [R,Hq] f64, pairs [R,Hq] i64)``.
+    """
+    lib = _load()
+    G = num_q_heads // num_kv_heads
+    if G > 64 or num_q_heads % num_kv_heads:
+        raise ValueError("oracle supports Hq % Hkv == 0 and G <= 64")
+    rows = _i32(rows)
+    R = int(rows.shape[0])
+    out = np.zeros((R, num_q_heads, head_dim), np.float64)
+    lse = np.zeros((R, num_q_heads), np.float64)
+    pairs = np.zeros((R, num_q_heads), np.int64)
+    arrs = [np.ascontiguousarray(a) if a is not None else None for a in (q, k_new, v_new, k_pool, v_pool)]
+    bt = _i32(block_table)
+    cu = _i32(cu_seqlens_q)
+    cl = _i32(cache_len)
+    rc = lib.csr_oracle_attention(
+        dtype, num_q_heads, num_kv_heads, head_dim, page_size, 0.0 if scale is None else float(scale),
+        int(cu.shape[0] - 1), *[_ptr(a) for a in arrs], _ptr(bt), int(bt_stride), _ptr(cu), _ptr(cl),
+        R, _ptr(rows), _ptr(out), _ptr(lse), _ptr(pairs), int(nthreads or default_threads()))
+    if rc != 0:
+        raise RuntimeError(f"oracle attention failed ({rc})")
+    return out, lse, pairs
+
+
+def kv_append(k_new, v_new, k_pool, v_pool, block_table, bt_stride, cu_seqlens_q, cache_len,
+              num_kv_heads, head_dim, page_size):
+    """Append oracle, in place on copies: Theorem 2's T (+) dX as a bit copy of
+    each chunk row into cache position L_b + i.  Returns the new pools."""
+    lib = _load()
+    kp = np.array(k_pool, copy=True)
+    vp = np.array(v_pool, copy=True)
+    kn = np.ascontiguousarray(k_new)
+    vn = np.ascontiguousarray(v_new)
+    bt = _i32(block_table)
+    cu = _i32(cu_seqlens_q)
+    cl = _i32(cache_len)
+    rc = lib.csr_oracle_kv_append(kn.itemsize, num_kv_heads, head_dim, page_size, int(cu.shape[0] - 1),
+                                  _ptr(kn), _ptr(vn), _ptr(kp), _ptr(vp), _ptr(bt), int(bt_stride),
+                                  _ptr(cu), _ptr(cl))
+    if rc != 0:
+        raise RuntimeError("oracle append failed")
+    return kp, vp
