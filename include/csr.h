@@ -1,0 +1,162 @@
+/*
+ * csr.h - C ABI of libcsr: cached-prefix extend attention for Cached State
+ * Representations (CSR) on AMD MI355X (gfx950).
+ *
+ * The operation (paper Sec. II, eq. (causal_attention_1)-(causal_attention_3),
+ * with the KV cache of eq. (K_cache)-(V_cache)): a chunk of n_b new query tokens
+ * of sequence b sits at absolute positions L_b .. L_b + n_b - 1 behind a cached
+ * prefix of L_b tokens.  For chunk row i, query head h and kv head
+ * g = h / (Hq / Hkv):
+ *     keys t = 0 .. L_b + i (inclusive; prefix fully visible, causal inside
+ *     the chunk), k_t / v_t from the paged cache for t < L_b and from the
+ *     chunk's own K/V rows for t >= L_b;
+ *     o = softmax(scale * q K^T) V,  lse = ln sum_t exp(scale * <q, k_t>).
+ * L_b is the reused-prefix length of the paper's CSR structure: i* = L_b + 1
+ * (eq. (csr_i_star)), i.e. the static part X_static is cached and the chunk is
+ * the new state chunk plus the dynamic suffix X_dyn.  L_b = 0 is the full
+ * re-prefill that asynchronous state reconciliation runs at eviction
+ * (Algorithm 1, warm-up; Theorem 4).
+ *
+ * Memory layout (all row-major, element type per csr_attn_desc.dtype):
+ *   q                 [T_q][Hq][d]        T_q = cu_seqlens_q[batch]
+ *   k_new, v_new      [T_q][Hkv][d]
+ *   out               [T_q][Hq][d]        same element type as q
+ *   lse               [T_q][Hq]           float (natural log), optional
+ *   k_pool, v_pool    [num_pages][P][Hkv][d]
+ *   block_table       [batch][bt_stride]  int32 page ids
+ * Position t of sequence b lives in pool slot page * P + t % P with
+ * page = block_table[b * bt_stride + t / P].  A NULL block_table means the
+ * contiguous cache page = b * bt_stride + t / P.
+ *
+ * Ownership: every pointer belongs to the caller.  Array arguments are device
+ * pointers (HIP device memory) unless stated otherwise; integers passed by
+ * value are host values, so no call synchronises with the device.  The library
+ * allocates no memory; split-K partials live in the caller's workspace.
+ *
+ * Streams: every call enqueues its kernels on `stream` (a hipStream_t passed
+ * as void*, NULL = the default stream) and returns without waiting.
+ *
+ * Errors: arguments are validated on the host before any HIP runtime call;
+ * a failed check returns CSR_E_INVAL / CSR_E_UNSUPPORTED / CSR_E_WORKSPACE and
+ * enqueues nothing.  A launch error returns CSR_E_HIP.  csr_last_error() gives
+ * a thread-local description of the last failure.  Block-table contents are a
+ * caller contract: every page a call touches must be a valid id in
+ * [0, num_pages); ids outside that range are neither read nor written (the key
+ * is taken as zero, the append row is dropped) so a bad table cannot fault the
+ * GPU, but the result is then unspecified.
+ */
+#ifndef CSR_H
+#define CSR_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  CSR_OK = 0,
+  CSR_E_INVAL = 1,        /* malformed argument (null pointer, bad size, misalignment) */
+  CSR_E_UNSUPPORTED = 2,  /* well-formed but not implemented (head_dim, dtype) */
+  CSR_E_WORKSPACE = 3,    /* workspace missing or smaller than the query says */
+  CSR_E_HIP = 4           /* HIP runtime reported an error at launch */
+} csr_status;
+
+typedef enum { CSR_F32 = 0, CSR_BF16 = 1 } csr_dtype;
+
+/* csr_extend_attention flags */
+#define CSR_APPEND 1u /* also append the chunk's K/V to the cache (csr_kv_append) */
+
+/* Attention geometry shared by every call. */
+typedef struct {
+  int32_t num_q_heads;   /* Hq >= 1 */
+  int32_t num_kv_heads;  /* Hkv >= 1, Hq % Hkv == 0 (grouped-query attention, G = Hq/Hkv) */
+  int32_t head_dim;      /* d: 64 or 128 */
+  int32_t page_size;     /* P: power of two, 1 .. 1024 */
+  float softmax_scale;   /* > 0, or 0 for 1/sqrt(d) (the paper's 1/sqrt(d_k)) */
+  int32_t dtype;         /* csr_dtype: CSR_BF16 (fp32 accumulate) or CSR_F32 */
+} csr_attn_desc;
+
+/*
+ * Append the chunk's keys and values to the paged cache: the paper's
+ * append-only growth T_{t+1} = T_t (+) dX_t (Theorem 2, eq.
+ * (incremental_extensibility)).  Chunk row i of sequence b (row
+ * cu_seqlens_q[b] + i of k_new / v_new) is copied bit for bit to cache
+ * position L_b + i, for every kv head.  No other byte of either pool changes,
+ * so every cached position < L_b stays as it was.  Committing the appended
+ * rows (advancing L_b) is the caller's choice: rows of the dynamic suffix are
+ * simply overwritten by the next call.
+ *   cu_seqlens_q   [batch+1] device int32 prefix sums of n_b
+ *   cache_seqlens  [batch] device int32 L_b, or NULL for all zero
+ *   total_q        host copy of cu_seqlens_q[batch]
+ *   num_pages      number of pages in each pool (bounds the writes)
+ * Pointers must be 16-byte aligned.
+ */
+csr_status csr_kv_append(const csr_attn_desc* desc, int32_t batch, const void* k_new,
+                         const void* v_new, void* k_pool, void* v_pool, int32_t num_pages,
+                         const int32_t* block_table, int32_t bt_stride,
+                         const int32_t* cu_seqlens_q, const int32_t* cache_seqlens,
+                         int32_t total_q, void* stream);
+
+/*
+ * Workspace bytes csr_extend_attention needs for these sizes (0 when the plan
+ * uses no split-K).  The same host integers must be passed to the call.
+ */
+size_t csr_extend_workspace_size(const csr_attn_desc* desc, int32_t batch, int32_t total_q,
+                                 int32_t max_seqlen_q, int32_t max_cache_len);
+
+/*
+ * Cached-prefix extend attention (see the file comment for the definition).
+ *   q, k_new, v_new   the chunk's projections, layouts above
+ *   k_pool, v_pool    the paged cache holding positions 0 .. L_b - 1; may be
+ *                     NULL only if max_cache_len == 0 and CSR_APPEND is unset
+ *   max_seqlen_q      host upper bound of n_b; max_cache_len host upper bound
+ *                     of L_b (they size the launch; exceeding them is an error
+ *                     the library cannot detect)
+ *   flags             CSR_APPEND: enqueue csr_kv_append first (the attention
+ *                     itself reads chunk keys from k_new / v_new either way)
+ *   out               [T_q][Hq][d], element type of q
+ *   lse               [T_q][Hq] float or NULL
+ *   workspace         device scratch of >= csr_extend_workspace_size() bytes
+ *                     (may be NULL when that size is 0); contents on entry
+ *                     are ignored
+ * Results are bitwise deterministic for a fixed set of host arguments.
+ */
+csr_status csr_extend_attention(const csr_attn_desc* desc, int32_t batch, const void* q,
+                                const void* k_new, const void* v_new, void* k_pool, void* v_pool,
+                                int32_t num_pages, const int32_t* block_table, int32_t bt_stride,
+                                const int32_t* cu_seqlens_q, const int32_t* cache_seqlens,
+                                int32_t total_q, int32_t max_seqlen_q, int32_t max_cache_len,
+                                uint32_t flags, void* out, float* lse, void* workspace,
+                                size_t workspace_bytes, void* stream);
+
+/* Workspace bytes csr_prefill needs (0 when the plan uses no split-K). */
+size_t csr_prefill_workspace_size(const csr_attn_desc* desc, int32_t batch, int32_t total,
+                                  int32_t max_seqlen);
+
+/*
+ * Full causal re-prefill, L_b = 0 for every sequence: the warm-up that
+ * recomputes the KV cache of the evicted state from scratch (i* = 1) in
+ * asynchronous state reconciliation (Algorithm 1; Theorem 4, warm-up time).
+ * Same computation as csr_extend_attention with no cached prefix.  If k_pool
+ * is non-NULL the sequence's K/V are also written to the cache at positions
+ * 0 .. n_b - 1 (the warmed-up cache), exactly as csr_kv_append with L_b = 0.
+ */
+csr_status csr_prefill(const csr_attn_desc* desc, int32_t batch, const void* q, const void* k,
+                       const void* v, void* k_pool, void* v_pool, int32_t num_pages,
+                       const int32_t* block_table, int32_t bt_stride, const int32_t* cu_seqlens,
+                       int32_t total, int32_t max_seqlen, void* out, float* lse, void* workspace,
+                       size_t workspace_bytes, void* stream);
+
+/* Static name of a status code. */
+const char* csr_status_string(csr_status status);
+
+/* Thread-local description of the last failure on this thread ("" if none). */
+const char* csr_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* CSR_H */

@@ -1,0 +1,161 @@
+"""Thin ctypes binding of libcsr (include/csr.h).
+
+Argument marshalling only: tensors are passed as raw device pointers, host
+integers by value, and the stream is torch's current HIP stream.  Every step of
+the computation runs in the library's HIP kernels.  The library must have been
+built (``python -m paper_2605_07325_amd.build``); there is no fallback.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import Optional
+
+import torch
+
+_LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libcsr.so")
+
+CSR_OK, CSR_E_INVAL, CSR_E_UNSUPPORTED, CSR_E_WORKSPACE, CSR_E_HIP = 0, 1, 2, 3, 4
+CSR_F32, CSR_BF16 = 0, 1
+CSR_APPEND = 1
+
+# Every function include/csr.h declares.
+EXPORTS = ("csr_kv_append", "csr_extend_workspace_size", "csr_extend_attention", "csr_prefill_workspace_size",
+           "csr_prefill", "csr_status_string", "csr_last_error")
+
+
+class AttnDesc(ctypes.Structure):
+    _fields_ = [("num_q_heads", ctypes.c_int32), ("num_kv_heads", ctypes.c_int32), ("head_dim", ctypes.c_int32),
+                ("page_size", ctypes.c_int32), ("softmax_scale", ctypes.c_float), ("dtype", ctypes.c_int32)]
+
+
+class CsrError(RuntimeError):
+    def __init__(self, status: int, message: str):
+        super().__init__(f"{_status_name(status)}: {message}")
+        self.status = status
+
+
+_lib = None
+
+
+def lib() -> ctypes.CDLL:
+    global _lib
+    if _lib is None:
+        if not os.path.exists(_LIB_PATH):
+            raise RuntimeError(f"{_LIB_PATH} is missing: build it with `python -m paper_2605_07325_amd.build`")
+        L = ctypes.CDLL(_LIB_PATH)
+        p, i32, u32, sz = ctypes.c_void_p, ctypes.c_int32, ctypes.c_uint32, ctypes.c_size_t
+        D = ctypes.POINTER(AttnDesc)
+        L.csr_kv_append.argtypes = [D, i32, p, p, p, p, i32, p, i32, p, p, i32, p]
+        L.csr_kv_append.restype = ctypes.c_int
+        L.csr_extend_workspace_size.argtypes = [D, i32, i32, i32, i32]
+        L.csr_extend_workspace_size.restype = sz
+        L.csr_extend_attention.argtypes = [D, i32, p, p, p, p, p, i32, p, i32, p, p, i32, i32, i32, u32, p, p, p, sz, p]
+        L.csr_extend_attention.restype = ctypes.c_int
+        L.csr_prefill_workspace_size.argtypes = [D, i32, i32, i32]
+        L.csr_prefill_workspace_size.restype = sz
+        L.csr_prefill.argtypes = [D, i32, p, p, p, p, p, i32, p, i32, p, i32, i32, p, p, p, sz, p]
+        L.csr_prefill.restype = ctypes.c_int
+        L.csr_status_string.argtypes = [ctypes.c_int]
+        L.csr_status_string.restype = ctypes.c_char_p
+        L.csr_last_error.argtypes = []
+        L.csr_last_error.restype = ctypes.c_char_p
+        _lib = L
+    return _lib
+
+
+def _status_name(st: int) -> str:
+    try:
+        return lib().csr_status_string(st).decode()
+    except Exception:  # library not loadable: still report the number
+        return f"status {st}"
+
+
+def _check(st: int) -> None:
+    if st != CSR_OK:
+        raise CsrError(st, lib().csr_last_error().decode())
+
+
+def make_desc(num_q_heads: int, num_kv_heads: int, head_dim: int, page_size: int = 16, dtype=torch.bfloat16,
+              softmax_scale: float = 0.0) -> AttnDesc:
+    dt = {torch.bfloat16: CSR_BF16, torch.float32: CSR_F32}.get(dtype, dtype)
+    return AttnDesc(num_q_heads, num_kv_heads, head_dim, page_size, softmax_scale, int(dt))
+
+
+def _ptr(t: Optional[torch.Tensor]):
+    return None if t is None else ctypes.c_void_p(t.data_ptr())
+
+
+def _stream(stream) -> ctypes.c_void_p:
+    if stream is None:
+        stream = torch.cuda.current_stream()
+    return ctypes.c_void_p(stream.cuda_stream if hasattr(stream, "cuda_stream") else int(stream))
+
+
+def _pages(pool: Optional[torch.Tensor]) -> int:
+    return 0 if pool is None else int(pool.shape[0])
+
+
+def kv_append(desc: AttnDesc, k_new, v_new, k_pool, v_pool, block_table, bt_stride: int, cu_seqlens_q,
+              cache_seqlens, stream=None) -> None:
+    """csr_kv_append: copy chunk K/V rows to cache positions L_b + i."""
+    batch = int(cu_seqlens_q.shape[0]) - 1
+    _check(lib().csr_kv_append(ctypes.byref(desc), batch, _ptr(k_new), _ptr(v_new), _ptr(k_pool), _ptr(v_pool),
+                               _pages(k_pool), _ptr(block_table), bt_stride, _ptr(cu_seqlens_q), _ptr(cache_seqlens),
+                               int(k_new.shape[0]), _stream(stream)))
+
+
+def extend_workspace_size(desc: AttnDesc, batch: int, total_q: int, max_seqlen_q: int, max_cache_len: int) -> int:
+    return int(lib().csr_extend_workspace_size(ctypes.byref(desc), batch, total_q, max_seqlen_q, max_cache_len))
+
+
+def prefill_workspace_size(desc: AttnDesc, batch: int, total: int, max_seqlen: int) -> int:
+    return int(lib().csr_prefill_workspace_size(ctypes.byref(desc), batch, total, max_seqlen))
+
+
+def _workspace(nbytes: int, device, workspace):
+    if nbytes == 0:
+        return workspace
+    if workspace is None or workspace.numel() * workspace.element_size() < nbytes:
+        workspace = torch.empty(nbytes, dtype=torch.uint8, device=device)
+    return workspace
+
+
+def extend_attention(desc: AttnDesc, q, k_new, v_new, k_pool, v_pool, block_table, bt_stride: int, cu_seqlens_q,
+                     cache_seqlens, max_seqlen_q: int, max_cache_len: int, append: bool = False, out=None,
+                     lse: Optional[torch.Tensor] = None, want_lse: bool = True, workspace=None, stream=None):
+    """csr_extend_attention.  Returns ``(out, lse)``; buffers are allocated with
+    torch when not supplied (lse only if ``want_lse``)."""
+    batch = int(cu_seqlens_q.shape[0]) - 1
+    total_q = int(q.shape[0])
+    if out is None:
+        out = torch.empty_like(q)
+    if lse is None and want_lse:
+        lse = torch.empty((total_q, desc.num_q_heads), dtype=torch.float32, device=q.device)
+    ws_bytes = extend_workspace_size(desc, batch, total_q, max_seqlen_q, max_cache_len) if total_q else 0
+    workspace = _workspace(ws_bytes, q.device, workspace)
+    ws_cap = 0 if workspace is None else workspace.numel() * workspace.element_size()
+    _check(lib().csr_extend_attention(
+        ctypes.byref(desc), batch, _ptr(q), _ptr(k_new), _ptr(v_new), _ptr(k_pool), _ptr(v_pool), _pages(k_pool),
+        _ptr(block_table), bt_stride, _ptr(cu_seqlens_q), _ptr(cache_seqlens), total_q, max_seqlen_q, max_cache_len,
+        CSR_APPEND if append else 0, _ptr(out), _ptr(lse), _ptr(workspace), ws_cap, _stream(stream)))
+    return out, lse
+
+
+def prefill(desc: AttnDesc, q, k, v, cu_seqlens, max_seqlen: int, k_pool=None, v_pool=None, block_table=None,
+            bt_stride: int = 1, out=None, lse=None, want_lse: bool = True, workspace=None, stream=None):
+    """csr_prefill (L = 0 re-prefill; optional warm-up write of the cache)."""
+    batch = int(cu_seqlens.shape[0]) - 1
+    total = int(q.shape[0])
+    if out is None:
+        out = torch.empty_like(q)
+    if lse is None and want_lse:
+        lse = torch.empty((total, desc.num_q_heads), dtype=torch.float32, device=q.device)
+    ws_bytes = prefill_workspace_size(desc, batch, total, max_seqlen) if total else 0
+    workspace = _workspace(ws_bytes, q.device, workspace)
+    ws_cap = 0 if workspace is None else workspace.numel() * workspace.element_size()
+    _check(lib().csr_prefill(
+        ctypes.byref(desc), batch, _ptr(q), _ptr(k), _ptr(v), _ptr(k_pool), _ptr(v_pool), _pages(k_pool),
+        _ptr(block_table), bt_stride, _ptr(cu_seqlens), total, max_seqlen, _ptr(out), _ptr(lse), _ptr(workspace),
+        ws_cap, _stream(stream)))
+    return out, lse

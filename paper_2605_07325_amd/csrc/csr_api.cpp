@@ -1,0 +1,354 @@
+// C ABI of libcsr (declared in include/csr.h): host-side validation, launch
+// planning and kernel launches on the caller's stream.
+//
+// Validation runs entirely on the host and precedes every HIP runtime call,
+// so malformed arguments are rejected without touching the device.
+#include <math.h>
+#include <stdarg.h>
+#include <stdint.h>
+#include <stdio.h>
+#include <stdlib.h>
+
+#include <string>
+
+#include "../../include/csr.h"
+#include "kernels.h"
+
+namespace {
+
+thread_local std::string g_last_error;
+
+csr_status fail(csr_status st, const char* fmt, ...) __attribute__((format(printf, 2, 3)));
+csr_status fail(csr_status st, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof buf, fmt, ap);
+  va_end(ap);
+  g_last_error = buf;
+  return st;
+}
+
+bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+bool aligned4(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 3u) == 0; }
+
+int ilog2(int x) {
+  int r = 0;
+  while ((1 << r) < x) ++r;
+  return r;
+}
+
+csr_status check_desc(const csr_attn_desc* d) {
+  if (!d) return fail(CSR_E_INVAL, "desc is NULL");
+  if (d->num_q_heads < 1 || d->num_kv_heads < 1)
+    return fail(CSR_E_INVAL, "head counts must be >= 1 (Hq=%d, Hkv=%d)", d->num_q_heads, d->num_kv_heads);
+  if (d->num_q_heads % d->num_kv_heads)
+    return fail(CSR_E_INVAL, "num_q_heads (%d) must be a multiple of num_kv_heads (%d)", d->num_q_heads,
+                d->num_kv_heads);
+  if (d->dtype != CSR_BF16 && d->dtype != CSR_F32) return fail(CSR_E_UNSUPPORTED, "unsupported dtype %d", d->dtype);
+  if (d->head_dim != 64 && d->head_dim != 128)
+    return fail(CSR_E_UNSUPPORTED, "head_dim %d unsupported (64 or 128)", d->head_dim);
+  if (d->page_size < 1 || d->page_size > 1024 || (d->page_size & (d->page_size - 1)))
+    return fail(CSR_E_INVAL, "page_size %d must be a power of two in [1, 1024]", d->page_size);
+  if (!(d->softmax_scale >= 0.f) || isinf(d->softmax_scale))
+    return fail(CSR_E_INVAL, "softmax_scale must be finite and >= 0 (0 = 1/sqrt(d))");
+  return CSR_OK;
+}
+
+int elem_bytes(const csr_attn_desc* d) { return d->dtype == CSR_BF16 ? 2 : 4; }
+
+// Launch plan: row tiles, key splits, workspace.  Pure function of the host
+// integers and the device's CU count, so the size query and the call agree.
+struct Plan {
+  int bm, mtiles, nsplit, n_units, xcd_remap;
+  size_t ws_o, ws_lse, ws_bytes;
+};
+
+int device_cus() {
+  int dev = 0, cus = 0;
+  if (hipGetDevice(&dev) != hipSuccess) return 256;
+  if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || cus <= 0) {
+    (void)hipGetLastError();
+    return 256;
+  }
+  return cus;
+}
+
+csr_status make_plan(const csr_attn_desc* d, int batch, int total_q, int max_q, int max_L, Plan& p) {
+  const int G = d->num_q_heads / d->num_kv_heads;
+  p.bm = csr::attn_block_m(d->dtype == CSR_BF16, d->head_dim);
+  const int64_t rows = (int64_t)max_q * G;
+  if (rows >= (1ll << 30) || (int64_t)max_L + max_q >= (1ll << 30))
+    return fail(CSR_E_UNSUPPORTED, "sequence too long (max_seqlen_q*G=%lld, max_cache_len+max_seqlen_q=%lld)",
+                (long long)rows, (long long)max_L + max_q);
+  p.mtiles = (int)((rows + p.bm - 1) / p.bm);
+  const int64_t base = (int64_t)batch * d->num_kv_heads * p.mtiles;
+  const int ntiles = (max_L + max_q + 63) / 64;
+  int nsplit = 1;
+  const char* env = getenv("CSR_NSPLIT");  // tuning override
+  if (env && atoi(env) > 0) {
+    nsplit = atoi(env);
+  } else {
+    const int cus = device_cus();
+    if (base > 0 && base < cus) {
+      nsplit = (int)((cus + base - 1) / base);
+      const int cap = ntiles / 8 > 1 ? ntiles / 8 : 1;  // keep >= 8 key tiles per split
+      if (nsplit > cap) nsplit = cap;
+    }
+  }
+  if (nsplit > ntiles) nsplit = ntiles > 0 ? ntiles : 1;
+  if (nsplit < 1) nsplit = 1;
+  p.nsplit = nsplit;
+  const int64_t units = base * nsplit;
+  if (units >= (1ll << 31) - 8) return fail(CSR_E_UNSUPPORTED, "too many work units (%lld)", (long long)units);
+  p.n_units = (int)units;
+  p.xcd_remap = max_L >= max_q ? 1 : 0;
+  if (nsplit > 1) {
+    const size_t rows_all = (size_t)total_q * d->num_q_heads;
+    p.ws_o = (size_t)nsplit * rows_all * d->head_dim * sizeof(float);
+    p.ws_lse = (size_t)nsplit * rows_all * sizeof(float);
+    p.ws_bytes = ((p.ws_o + 255) & ~(size_t)255) + p.ws_lse;
+  } else {
+    p.ws_o = p.ws_lse = p.ws_bytes = 0;
+  }
+  return CSR_OK;
+}
+
+csr_status check_common(const csr_attn_desc* d, int batch, int total, const void* q, const void* k,
+                        const void* v, void* out, float* lse, const int32_t* cu) {
+  csr_status st = check_desc(d);
+  if (st != CSR_OK) return st;
+  if (batch < 0 || total < 0) return fail(CSR_E_INVAL, "negative batch (%d) or token count (%d)", batch, total);
+  if (batch == 0 && total != 0) return fail(CSR_E_INVAL, "batch 0 with %d tokens", total);
+  if (total == 0) return CSR_OK;
+  if (!q || !k || !v || !out || !cu) return fail(CSR_E_INVAL, "q, k, v, out and cu_seqlens must be non-NULL");
+  if (!aligned16(q) || !aligned16(k) || !aligned16(v) || !aligned16(out))
+    return fail(CSR_E_INVAL, "q, k, v and out must be 16-byte aligned");
+  if (lse && !aligned4(lse)) return fail(CSR_E_INVAL, "lse must be 4-byte aligned");
+  if (!aligned4(cu)) return fail(CSR_E_INVAL, "cu_seqlens must be 4-byte aligned");
+  return CSR_OK;
+}
+
+csr_status check_pool(const csr_attn_desc* d, const void* k_pool, const void* v_pool, int num_pages,
+                      const int32_t* block_table, int bt_stride, int max_len, const char* what) {
+  (void)d;
+  if (!k_pool || !v_pool) return fail(CSR_E_INVAL, "%s: k_pool and v_pool must be non-NULL", what);
+  if (!aligned16(k_pool) || !aligned16(v_pool)) return fail(CSR_E_INVAL, "%s: pools must be 16-byte aligned", what);
+  if (num_pages < 1) return fail(CSR_E_INVAL, "%s: num_pages must be >= 1", what);
+  if (bt_stride < 1) return fail(CSR_E_INVAL, "%s: bt_stride must be >= 1", what);
+  if ((int64_t)bt_stride * d->page_size < max_len)
+    return fail(CSR_E_INVAL, "%s: bt_stride %d pages of %d cannot hold %d positions", what, bt_stride,
+                d->page_size, max_len);
+  if (block_table && !aligned4(block_table)) return fail(CSR_E_INVAL, "%s: block_table must be 4-byte aligned", what);
+  return CSR_OK;
+}
+
+csr_status launched(hipError_t e, const char* what) {
+  if (e != hipSuccess) return fail(CSR_E_HIP, "%s launch failed: %s", what, hipGetErrorString(e));
+  return CSR_OK;
+}
+
+csr::AppendArgs append_args(const csr_attn_desc* d, int batch, const void* k_new, const void* v_new, void* k_pool,
+                            void* v_pool, int num_pages, const int32_t* bt, int bt_stride, const int32_t* cu,
+                            const int32_t* cache_len, int total_q) {
+  csr::AppendArgs a;
+  a.k_new = k_new;
+  a.v_new = v_new;
+  a.k_pool = k_pool;
+  a.v_pool = v_pool;
+  a.block_table = bt;
+  a.cu_q = cu;
+  a.cache_len = cache_len;
+  a.num_pages = num_pages;
+  a.bt_stride = bt_stride;
+  a.batch = batch;
+  a.total_q = total_q;
+  a.Hkv = d->num_kv_heads;
+  a.P = d->page_size;
+  a.log2P = ilog2(d->page_size);
+  a.row_chunks = d->head_dim * elem_bytes(d) / 16;
+  return a;
+}
+
+// Shared body of extend attention and prefill (cache_len == NULL, max_L == 0).
+csr_status run_attention(const csr_attn_desc* d, int batch, const void* q, const void* k_new, const void* v_new,
+                         const void* k_pool, const void* v_pool, int num_pages, const int32_t* bt, int bt_stride,
+                         const int32_t* cu, const int32_t* cache_len, int total_q, int max_q, int max_L, void* out,
+                         float* lse, void* ws, size_t ws_bytes, hipStream_t stream) {
+  Plan p;
+  csr_status st = make_plan(d, batch, total_q, max_q, max_L, p);
+  if (st != CSR_OK) return st;
+  if (p.ws_bytes > 0) {
+    if (!ws) return fail(CSR_E_WORKSPACE, "workspace of %zu bytes required, got NULL", p.ws_bytes);
+    if (ws_bytes < p.ws_bytes)
+      return fail(CSR_E_WORKSPACE, "workspace of %zu bytes required, got %zu", p.ws_bytes, ws_bytes);
+    if (!aligned16(ws)) return fail(CSR_E_INVAL, "workspace must be 16-byte aligned");
+  }
+  const int G = d->num_q_heads / d->num_kv_heads;
+  const float scale = d->softmax_scale > 0.f ? d->softmax_scale : 1.f / sqrtf((float)d->head_dim);
+  csr::AttnArgs a;
+  a.q = q;
+  a.k_new = k_new;
+  a.v_new = v_new;
+  a.k_pool = k_pool;
+  a.v_pool = v_pool;
+  a.block_table = bt;
+  a.cu_q = cu;
+  a.cache_len = cache_len;
+  a.out = out;
+  a.lse = lse;
+  a.part_o = p.nsplit > 1 ? static_cast<float*>(ws) : nullptr;
+  a.part_lse = p.nsplit > 1 ? reinterpret_cast<float*>(static_cast<char*>(ws) + ((p.ws_o + 255) & ~(size_t)255))
+                            : nullptr;
+  a.num_pages = num_pages;
+  a.bt_stride = bt_stride;
+  a.Hq = d->num_q_heads;
+  a.Hkv = d->num_kv_heads;
+  a.G = G;
+  a.d = d->head_dim;
+  a.P = d->page_size;
+  a.log2P = ilog2(d->page_size);
+  a.scale_log2 = scale * 1.4426950408889634f;
+  a.batch = batch;
+  a.total_q = total_q;
+  a.mtiles = p.mtiles;
+  a.nsplit = p.nsplit;
+  a.n_units = p.n_units;
+  a.xcd_remap = p.xcd_remap;
+  st = launched(csr::launch_attention(a, d->dtype == CSR_BF16, stream), "attention");
+  if (st != CSR_OK || p.nsplit == 1) return st;
+  csr::MergeArgs m;
+  m.part_o = a.part_o;
+  m.part_lse = a.part_lse;
+  m.out = out;
+  m.lse = lse;
+  m.nsplit = p.nsplit;
+  m.total_q = total_q;
+  m.Hq = d->num_q_heads;
+  m.d = d->head_dim;
+  return launched(csr::launch_merge(m, d->dtype == CSR_BF16, stream), "split-K merge");
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* csr_status_string(csr_status s) {
+  switch (s) {
+    case CSR_OK: return "CSR_OK";
+    case CSR_E_INVAL: return "CSR_E_INVAL";
+    case CSR_E_UNSUPPORTED: return "CSR_E_UNSUPPORTED";
+    case CSR_E_WORKSPACE: return "CSR_E_WORKSPACE";
+    case CSR_E_HIP: return "CSR_E_HIP";
+  }
+  return "CSR_E_UNKNOWN";
+}
+
+const char* csr_last_error(void) { return g_last_error.c_str(); }
+
+csr_status csr_kv_append(const csr_attn_desc* desc, int32_t batch, const void* k_new, const void* v_new,
+                         void* k_pool, void* v_pool, int32_t num_pages, const int32_t* block_table,
+                         int32_t bt_stride, const int32_t* cu_seqlens_q, const int32_t* cache_seqlens,
+                         int32_t total_q, void* stream) {
+  g_last_error.clear();
+  csr_status st = check_desc(desc);
+  if (st != CSR_OK) return st;
+  if (batch < 0 || total_q < 0) return fail(CSR_E_INVAL, "negative batch or total_q");
+  if (total_q == 0) return CSR_OK;
+  if (batch == 0) return fail(CSR_E_INVAL, "batch 0 with %d tokens", total_q);
+  if (!k_new || !v_new || !cu_seqlens_q) return fail(CSR_E_INVAL, "k_new, v_new and cu_seqlens_q must be non-NULL");
+  if (!aligned16(k_new) || !aligned16(v_new)) return fail(CSR_E_INVAL, "k_new and v_new must be 16-byte aligned");
+  st = check_pool(desc, k_pool, v_pool, num_pages, block_table, bt_stride, 0, "kv_append");
+  if (st != CSR_OK) return st;
+  if (cache_seqlens && !aligned4(cache_seqlens)) return fail(CSR_E_INVAL, "cache_seqlens must be 4-byte aligned");
+  const csr::AppendArgs a = append_args(desc, batch, k_new, v_new, k_pool, v_pool, num_pages, block_table, bt_stride,
+                                        cu_seqlens_q, cache_seqlens, total_q);
+  return launched(csr::launch_append(a, static_cast<hipStream_t>(stream)), "kv_append");
+}
+
+size_t csr_extend_workspace_size(const csr_attn_desc* desc, int32_t batch, int32_t total_q, int32_t max_seqlen_q,
+                                 int32_t max_cache_len) {
+  if (check_desc(desc) != CSR_OK || batch < 1 || total_q < 1 || max_seqlen_q < 1 || max_cache_len < 0) return 0;
+  Plan p;
+  if (make_plan(desc, batch, total_q, max_seqlen_q, max_cache_len, p) != CSR_OK) return 0;
+  return p.ws_bytes;
+}
+
+size_t csr_prefill_workspace_size(const csr_attn_desc* desc, int32_t batch, int32_t total, int32_t max_seqlen) {
+  return csr_extend_workspace_size(desc, batch, total, max_seqlen, 0);
+}
+
+csr_status csr_extend_attention(const csr_attn_desc* desc, int32_t batch, const void* q, const void* k_new,
+                                const void* v_new, void* k_pool, void* v_pool, int32_t num_pages,
+                                const int32_t* block_table, int32_t bt_stride, const int32_t* cu_seqlens_q,
+                                const int32_t* cache_seqlens, int32_t total_q, int32_t max_seqlen_q,
+                                int32_t max_cache_len, uint32_t flags, void* out, float* lse, void* workspace,
+                                size_t workspace_bytes, void* stream) {
+  g_last_error.clear();
+  csr_status st = check_common(desc, batch, total_q, q, k_new, v_new, out, lse, cu_seqlens_q);
+  if (st != CSR_OK || total_q == 0) return st;
+  if (flags & ~CSR_APPEND) return fail(CSR_E_INVAL, "unknown flags 0x%x", flags);
+  if (max_seqlen_q < 1 || max_cache_len < 0)
+    return fail(CSR_E_INVAL, "max_seqlen_q must be >= 1 and max_cache_len >= 0");
+  if (max_seqlen_q > total_q) return fail(CSR_E_INVAL, "max_seqlen_q %d exceeds total_q %d", max_seqlen_q, total_q);
+  const bool need_pool = max_cache_len > 0 || (flags & CSR_APPEND);
+  if (need_pool) {
+    // Each of L_b and n_b must fit a table row; their per-sequence sum is a
+    // caller contract (the host does not see the device-side lengths).
+    st = check_pool(desc, k_pool, v_pool, num_pages, block_table, bt_stride,
+                    max_cache_len > max_seqlen_q ? max_cache_len : max_seqlen_q, "extend_attention");
+    if (st != CSR_OK) return st;
+  }
+  if (max_cache_len > 0 && !cache_seqlens)
+    return fail(CSR_E_INVAL, "cache_seqlens must be non-NULL when max_cache_len > 0");
+  if (cache_seqlens && !aligned4(cache_seqlens)) return fail(CSR_E_INVAL, "cache_seqlens must be 4-byte aligned");
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  if (flags & CSR_APPEND) {
+    const csr::AppendArgs a = append_args(desc, batch, k_new, v_new, k_pool, v_pool, num_pages, block_table,
+                                          bt_stride, cu_seqlens_q, cache_seqlens, total_q);
+    // Validate the plan (workspace) before enqueuing anything.
+    Plan p;
+    st = make_plan(desc, batch, total_q, max_seqlen_q, max_cache_len, p);
+    if (st != CSR_OK) return st;
+    if (p.ws_bytes > 0 && (!workspace || workspace_bytes < p.ws_bytes))
+      return fail(CSR_E_WORKSPACE, "workspace of %zu bytes required, got %zu", p.ws_bytes,
+                  workspace ? workspace_bytes : (size_t)0);
+    st = launched(csr::launch_append(a, s), "kv_append");
+    if (st != CSR_OK) return st;
+  }
+  return run_attention(desc, batch, q, k_new, v_new, k_pool, v_pool, num_pages, block_table, bt_stride, cu_seqlens_q,
+                       max_cache_len > 0 ? cache_seqlens : nullptr, total_q, max_seqlen_q, max_cache_len, out, lse,
+                       workspace, workspace_bytes, s);
+}
+
+csr_status csr_prefill(const csr_attn_desc* desc, int32_t batch, const void* q, const void* k, const void* v,
+                       void* k_pool, void* v_pool, int32_t num_pages, const int32_t* block_table, int32_t bt_stride,
+                       const int32_t* cu_seqlens, int32_t total, int32_t max_seqlen, void* out, float* lse,
+                       void* workspace, size_t workspace_bytes, void* stream) {
+  g_last_error.clear();
+  csr_status st = check_common(desc, batch, total, q, k, v, out, lse, cu_seqlens);
+  if (st != CSR_OK || total == 0) return st;
+  if (max_seqlen < 1 || max_seqlen > total) return fail(CSR_E_INVAL, "max_seqlen must be in [1, total]");
+  const bool write_cache = k_pool != nullptr || v_pool != nullptr;
+  if (write_cache) {
+    st = check_pool(desc, k_pool, v_pool, num_pages, block_table, bt_stride, max_seqlen, "prefill");
+    if (st != CSR_OK) return st;
+  }
+  Plan p;
+  st = make_plan(desc, batch, total, max_seqlen, 0, p);
+  if (st != CSR_OK) return st;
+  if (p.ws_bytes > 0 && (!workspace || workspace_bytes < p.ws_bytes))
+    return fail(CSR_E_WORKSPACE, "workspace of %zu bytes required, got %zu", p.ws_bytes,
+                workspace ? workspace_bytes : (size_t)0);
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  if (write_cache) {
+    const csr::AppendArgs a = append_args(desc, batch, k, v, k_pool, v_pool, num_pages, block_table, bt_stride,
+                                          cu_seqlens, nullptr, total);
+    st = launched(csr::launch_append(a, s), "prefill cache write");
+    if (st != CSR_OK) return st;
+  }
+  return run_attention(desc, batch, q, k, v, nullptr, nullptr, 0, nullptr, 1, cu_seqlens, nullptr, total, max_seqlen,
+                       0, out, lse, workspace, workspace_bytes, s);
+}
+
+}  // extern "C"

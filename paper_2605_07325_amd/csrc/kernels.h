@@ -1,0 +1,61 @@
+// Internal launch interface between the C ABI (csr_api.cpp) and the HIP
+// kernels.  Not installed; the public interface is include/csr.h.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace csr {
+
+// Everything one attention launch needs.  Sizes are validated by the caller.
+struct AttnArgs {
+  const void* q;
+  const void* k_new;
+  const void* v_new;
+  const void* k_pool;
+  const void* v_pool;
+  const int32_t* block_table;
+  const int32_t* cu_q;
+  const int32_t* cache_len;  // nullptr: every L_b = 0
+  void* out;                 // final output (nsplit == 1)
+  float* lse;                // final lse or nullptr (nsplit == 1)
+  float* part_o;             // [nsplit][T_q][Hq][d] partial outputs (nsplit > 1)
+  float* part_lse;           // [nsplit][T_q][Hq]
+  int32_t num_pages;
+  int32_t bt_stride;
+  int32_t Hq, Hkv, G, d, P, log2P;
+  float scale_log2;          // softmax scale * log2(e)
+  int32_t batch, total_q;
+  int32_t mtiles;            // packed-row tiles per (sequence, kv head)
+  int32_t nsplit;            // key-range splits per tile
+  int32_t n_units;           // batch * Hkv * nsplit * mtiles
+  int32_t xcd_remap;         // 1: keep units that share K/V on one XCD
+};
+
+// Packed rows (query token x head-in-group) per workgroup for each kernel.
+int attn_block_m(int dtype_bf16, int d);
+hipError_t launch_attention(const AttnArgs& a, int dtype_bf16, hipStream_t stream);
+
+struct MergeArgs {
+  const float* part_o;
+  const float* part_lse;
+  void* out;
+  float* lse;
+  int32_t nsplit, total_q, Hq, d;
+};
+hipError_t launch_merge(const MergeArgs& a, int dtype_bf16, hipStream_t stream);
+
+struct AppendArgs {
+  const void* k_new;
+  const void* v_new;
+  void* k_pool;
+  void* v_pool;
+  const int32_t* block_table;
+  const int32_t* cu_q;
+  const int32_t* cache_len;  // nullptr: every L_b = 0
+  int32_t num_pages, bt_stride, batch, total_q, Hkv, P, log2P;
+  int32_t row_chunks;        // 16-byte chunks per (token, kv head) row = d * elem / 16
+};
+hipError_t launch_append(const AppendArgs& a, hipStream_t stream);
+
+}  // namespace csr
