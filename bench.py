@@ -1,0 +1,308 @@
+#!/usr/bin/env python3
+"""Benchmark of the CSR hot path on one MI355X: cached-prefix extend attention.
+
+A step is one pass of the whole path over one synthetic batch: the paged KV
+append of the new chunk, the extend attention over the cached prefix plus the
+chunk, and the split-K merge when the plan splits (csr_extend_attention with
+CSR_APPEND).  The default workload is one layer with a 122880-token cached
+prefix and a 512-token chunk, GQA 64 query / 4 kv heads, head_dim 128, bf16,
+page size 16.
+
+Timing: W untimed warm-up steps, then exactly K steps between two
+synchronisations, timed with events on the stream the library launches on.
+Consecutive steps read different copies of the K/V pool (three copies of about
+250 MB), so the 256 MB Infinity Cache cannot serve a step's prefix from the
+previous step.  The attention kernel's own duration is read live through the
+library's csr_set_attention_events hook.
+
+Prints one JSON line.  ``--gpus N`` with N > 1 is rejected: this build runs
+on one GPU.
+"""
+from __future__ import annotations
+
+import argparse
+import ctypes
+import hashlib
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+PEAK_BF16_TFLOPS = 2500.0   # MI355X dense bf16 MFMA (published)
+PEAK_F32_TFLOPS = 157.3     # MI355X fp32 matrix (published)
+PEAK_HBM_GBS = 8000.0       # MI355X HBM3E (published)
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic_extend_attn.json")
+KERNEL_SRC = os.path.join(ROOT, "paper_2605_07325_amd", "csrc", "extend_attn.hip")
+
+
+def log(msg):
+    print(f"[bench {time.strftime('%H:%M:%S')}] {msg}", file=sys.stderr, flush=True)
+
+
+def kernel_source_hash() -> str:
+    with open(KERNEL_SRC, "rb") as f:
+        return hashlib.sha256(f.read()).hexdigest()[:16]
+
+
+def measured_traffic(workload: str):
+    """HBM bytes per attention launch from the committed counter summary, or
+    None when no summary exists for this workload or the kernel source changed
+    since the counters were taken."""
+    try:
+        with open(TRAFFIC_FILE) as f:
+            rec = json.load(f)
+    except (OSError, ValueError):
+        return None
+    ent = rec.get(workload)
+    if not ent or ent.get("kernel_sha") != kernel_source_hash():
+        return None
+    return ent.get("bytes_per_launch")
+
+
+class HipEvents:
+    """Raw hipEvent_t handles (the same HIP runtime torch loaded)."""
+
+    def __init__(self):
+        self.hip = ctypes.CDLL("libamdhip64.so.7")
+        self.hip.hipEventCreate.argtypes = [ctypes.POINTER(ctypes.c_void_p)]
+        self.hip.hipEventElapsedTime.argtypes = [ctypes.POINTER(ctypes.c_float), ctypes.c_void_p, ctypes.c_void_p]
+        self.hip.hipEventDestroy.argtypes = [ctypes.c_void_p]
+
+    def create(self):
+        ev = ctypes.c_void_p()
+        if self.hip.hipEventCreate(ctypes.byref(ev)) != 0:
+            raise RuntimeError("hipEventCreate failed")
+        return ev.value
+
+    def elapsed_ms(self, a, b) -> float:
+        ms = ctypes.c_float()
+        if self.hip.hipEventElapsedTime(ctypes.byref(ms), ctypes.c_void_p(a), ctypes.c_void_p(b)) != 0:
+            raise RuntimeError("hipEventElapsedTime failed")
+        return float(ms.value)
+
+    def destroy(self, ev):
+        self.hip.hipEventDestroy(ctypes.c_void_p(ev))
+
+
+def cpu_baseline(case, target_s: float):
+    """The fp64 oracle timed on this host's cores on a bounded sample of the
+    same workload's query tokens (all heads of each sampled token)."""
+    from oracle import oracle
+    from paper_2605_07325_amd import datagen as dg
+
+    threads = oracle.default_threads()
+    L = case.cache_len.astype(np.int64)
+    n = case.seqlen_q.astype(np.int64)
+
+    def run(count):
+        rows = dg.sample_rows(case, count, seed=1, cfg_id=99)
+        t0 = time.perf_counter()
+        _, _, pairs = oracle.attention(oracle.BF16 if case.dtype == dg.BF16 else oracle.F32, case.q, case.k_new,
+                                       case.v_new, case.k_pool, case.v_pool, case.block_table, case.bt_stride,
+                                       case.cu_seqlens_q, case.cache_len, rows, case.num_q_heads,
+                                       case.num_kv_heads, case.head_dim, case.page_size, nthreads=threads)
+        dt = time.perf_counter() - t0
+        flops = 4 * case.head_dim * int(pairs.sum())
+        return len(rows), dt, flops
+
+    cnt, dt, fl = run(threads)  # probe: one token per thread
+    if dt < target_s / 2:
+        want = int(cnt * target_s / max(dt, 1e-3))
+        cnt, dt, fl = run(min(want, case.total_q))
+    tflops = fl / dt / 1e12
+    full_s = case.flops() / (fl / dt)
+    log(f"cpu baseline: {cnt} tokens x {case.num_q_heads} heads in {dt:.1f}s on {threads} threads "
+        f"({tflops * 1e3:.2f} GFLOP/s; full layer extrapolated {full_s:.0f}s)")
+    return {"value": tflops, "unit": "TFLOP/s", "cores": threads, "kind": "oracle",
+            "sample": (f"{cnt} of {case.total_q} query tokens, all {case.num_q_heads} heads, of the same workload "
+                       f"({fl / 1e9:.1f} GFLOP, {dt:.1f} s; full layer extrapolates to {full_s:.0f} s)")}
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--workload", default="c3_512",
+                    help="c3_<n> extend over a 122880 prefix (default n=512), c2, c5, c1, c4_<S> (prefill)")
+    ap.add_argument("--pools", type=int, default=3, help="K/V pool copies rotated across steps")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-seconds", type=float, default=15.0)
+    ap.add_argument("--no-prefill-ratio", action="store_true")
+    ap.add_argument("--copy-calibration", action="store_true",
+                    help="also run a 1 GiB device copy (HBM counter calibration for rocprofv3 --pmc runs)")
+    args = ap.parse_args()
+
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print(f"bench.py runs on one GPU only (asked for --gpus {args.gpus}, WORLD_SIZE={world}); "
+              "the multi-GPU sharding of this path is a design note, not a measured configuration.", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+
+    from paper_2605_07325_amd import csr
+    from paper_2605_07325_amd import datagen as dg
+
+    csr.lib()  # fail loudly if the HIP library is not built
+    if not torch.cuda.is_available():
+        print("bench.py needs an MI355X (no GPU visible)", file=sys.stderr)
+        sys.exit(1)
+
+    t0 = time.perf_counter()
+    case = dg.config(args.workload)
+    log(f"workload {args.workload}: L={case.cache_len.tolist()} n={case.seqlen_q.tolist()} "
+        f"Hq={case.num_q_heads} Hkv={case.num_kv_heads} d={case.head_dim} P={case.page_size} "
+        f"({time.perf_counter() - t0:.1f}s to generate)")
+    prefill_mode = int(case.cache_len.max()) == 0
+    bf16 = case.dtype == dg.BF16
+
+    def dev(a):
+        if bf16:
+            return torch.from_numpy(np.ascontiguousarray(a).view(np.int16)).view(torch.bfloat16).cuda()
+        return torch.from_numpy(np.ascontiguousarray(a)).cuda()
+
+    q, k_new, v_new = dev(case.q), dev(case.k_new), dev(case.v_new)
+    pools = [(dev(case.k_pool), dev(case.v_pool))]
+    for _ in range(max(1, args.pools) - 1):
+        pools.append((pools[0][0].clone(), pools[0][1].clone()))
+    bt = None if case.block_table is None else torch.from_numpy(case.block_table).cuda()
+    cu = torch.from_numpy(case.cu_seqlens_q).cuda()
+    cl = torch.from_numpy(case.cache_len).cuda()
+    desc = csr.make_desc(case.num_q_heads, case.num_kv_heads, case.head_dim, case.page_size,
+                         torch.bfloat16 if bf16 else torch.float32)
+    out = torch.empty_like(q)
+    lse = torch.empty((case.total_q, case.num_q_heads), dtype=torch.float32, device="cuda")
+    if prefill_mode:
+        ws_bytes = csr.prefill_workspace_size(desc, case.batch, case.total_q, case.max_seqlen_q)
+    else:
+        ws_bytes = csr.extend_workspace_size(desc, case.batch, case.total_q, case.max_seqlen_q, case.max_cache_len)
+    ws = torch.empty(max(ws_bytes, 16), dtype=torch.uint8, device="cuda")
+
+    def step(i):
+        kp, vp = pools[i % len(pools)]
+        if prefill_mode:
+            csr.prefill(desc, q, k_new, v_new, cu, case.max_seqlen_q, k_pool=kp, v_pool=vp, block_table=bt,
+                        bt_stride=case.bt_stride, out=out, lse=lse, workspace=ws)
+        else:
+            csr.extend_attention(desc, q, k_new, v_new, kp, vp, bt, case.bt_stride, cu, cl, case.max_seqlen_q,
+                                 case.max_cache_len, append=True, out=out, lse=lse, workspace=ws)
+
+    if args.copy_calibration:
+        src = torch.empty(1 << 30, dtype=torch.uint8, device="cuda")
+        dst = torch.empty_like(src)
+        src.fill_(1)
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        log("copy calibration: 1 GiB device-to-device copy done")
+        del src, dst
+
+    for i in range(args.warmup):
+        step(i)
+    torch.cuda.synchronize()
+    log(f"warmup {args.warmup} steps done")
+
+    hip = HipEvents()
+    evs = [(hip.create(), hip.create()) for _ in range(args.steps)]
+    start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    start.record()
+    for i in range(args.steps):
+        csr.set_attention_events(*evs[i])
+        step(args.warmup + i)
+    end.record()
+    csr.set_attention_events(None, None)
+    torch.cuda.synchronize()
+    total_ms = start.elapsed_time(end)
+    attn_ms = [hip.elapsed_ms(a, b) for a, b in evs]
+    for a, b in evs:
+        hip.destroy(a)
+        hip.destroy(b)
+    ms_per_step = total_ms / args.steps
+    attn_avg = float(np.mean(attn_ms))
+    flops = case.flops()
+    value = flops / (ms_per_step * 1e-3) / 1e12
+    peak = PEAK_BF16_TFLOPS if bf16 else PEAK_F32_TFLOPS
+    achieved = flops / (attn_avg * 1e-3) / 1e12
+    log(f"{args.steps} steps: {ms_per_step:.4f} ms/step ({value:.1f} TFLOP/s); attention kernel avg "
+        f"{attn_avg:.4f} ms (min {min(attn_ms):.4f}) = {achieved:.1f} TFLOP/s = {100 * achieved / peak:.1f}% of peak")
+    abytes = case.algorithmic_bytes(append=True)
+    traffic = measured_traffic(args.workload)
+    rec = {
+        "metric": "extend-attn TFLOP/s & ms/layer at 120K cached prefix, 512-tok chunk; % MFMA peak",
+        "value": round(value, 3),
+        "unit": "TFLOP/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 5),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16" if bf16 else "f32",
+        "data": "synthetic",
+        "config": {
+            "workload": (f"{'re-prefill' if prefill_mode else 'extend'} one layer: L={case.max_cache_len} cached "
+                         f"prefix, n={case.max_seqlen_q} chunk, batch {case.batch}, GQA {case.num_q_heads}q/"
+                         f"{case.num_kv_heads}kv, head_dim {case.head_dim}, page {case.page_size}, "
+                         f"{'kv append + ' if not prefill_mode else 'cache write + '}attention (+ split-K merge)"),
+            "name": args.workload,
+            "global_batch": case.batch,
+            "seq_len": int(case.max_cache_len + case.max_seqlen_q),
+            "chunk_tokens": case.total_q,
+            "gflop_per_step": round(flops / 1e9, 2),
+            "algorithmic_mb_per_step": round(abytes / 1e6, 2),
+            "pool_copies_rotated": len(pools),
+        },
+        "roofline": {
+            "bound": "mfma",
+            "achieved": round(achieved, 3),
+            "peak": peak,
+            "unit": "TFLOP/s",
+            "frac": round(achieved / peak, 4),
+            "traffic": traffic,
+            "kernel": "attn_bf16_kernel" if bf16 else "attn_f32_kernel",
+            "kernel_ms": round(attn_avg, 5),
+            "hbm_gbs_algorithmic": round(abytes / (attn_avg * 1e-3) / 1e9, 1),
+        },
+    }
+    if not prefill_mode and not args.no_prefill_ratio and bf16:
+        S = int(case.cache_len[0] + case.seqlen_q[0])
+        g = torch.Generator(device="cuda")
+        g.manual_seed(7)
+        qq = (torch.randn((S, case.num_q_heads, case.head_dim), device="cuda", generator=g) * 0.5).to(torch.bfloat16)
+        kk = (torch.randn((S, case.num_kv_heads, case.head_dim), device="cuda", generator=g) * 0.5).to(torch.bfloat16)
+        vv = (torch.randn((S, case.num_kv_heads, case.head_dim), device="cuda", generator=g) * 0.5).to(torch.bfloat16)
+        cu2 = torch.tensor([0, S], dtype=torch.int32, device="cuda")
+        o2 = torch.empty_like(qq)
+        ws2 = torch.empty(max(16, csr.prefill_workspace_size(desc, 1, S, S)), dtype=torch.uint8, device="cuda")
+        csr.prefill(desc, qq, kk, vv, cu2, S, out=o2, want_lse=False, workspace=ws2)
+        torch.cuda.synchronize()
+        reps = 3
+        s2, e2 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        s2.record()
+        for _ in range(reps):
+            csr.prefill(desc, qq, kk, vv, cu2, S, out=o2, want_lse=False, workspace=ws2)
+        e2.record()
+        torch.cuda.synchronize()
+        pms = s2.elapsed_time(e2) / reps
+        pflops = 4 * case.head_dim * case.num_q_heads * S * (S + 1) // 2
+        rec["reprefill_same_history"] = {
+            "tokens": S, "ms": round(pms, 3), "tflops": round(pflops / (pms * 1e-3) / 1e12, 1),
+            "time_ratio_vs_extend_step": round(pms / ms_per_step, 1),
+            "flop_ratio": round(pflops / flops, 1),
+        }
+        log(f"re-prefill of the same {S}-token history: {pms:.2f} ms ({pms / ms_per_step:.1f}x the extend step)")
+        del qq, kk, vv, o2, ws2
+    if not args.no_cpu_baseline:
+        rec["cpu_baseline"] = cpu_baseline(case, args.cpu_seconds)
+    print(json.dumps(rec), flush=True)
+
+
+if __name__ == "__main__":
+    main()

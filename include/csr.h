@@ -149,6 +149,17 @@ csr_status csr_prefill(const csr_attn_desc* desc, int32_t batch, const void* q, 
                        int32_t total, int32_t max_seqlen, void* out, float* lse, void* workspace,
                        size_t workspace_bytes, void* stream);
 
+/*
+ * Timing hook for profilers and benchmarks.  While set, every later
+ * csr_extend_attention / csr_prefill call made on this thread enqueues
+ * hipEventRecord(begin_event) immediately before its attention kernel and
+ * hipEventRecord(end_event) immediately after it, on the call's stream, so the
+ * caller can read that kernel's duration with hipEventElapsedTime.  The events
+ * are hipEvent_t handles owned by the caller; pass NULL, NULL to switch the
+ * hook off.  Returns CSR_E_INVAL if exactly one of them is NULL.
+ */
+csr_status csr_set_attention_events(void* begin_event, void* end_event);
+
 /* Static name of a status code. */
 const char* csr_status_string(csr_status status);
 

@@ -21,7 +21,7 @@ CSR_APPEND = 1
 
 # Every function include/csr.h declares.
 EXPORTS = ("csr_kv_append", "csr_extend_workspace_size", "csr_extend_attention", "csr_prefill_workspace_size",
-           "csr_prefill", "csr_status_string", "csr_last_error")
+           "csr_prefill", "csr_set_attention_events", "csr_status_string", "csr_last_error")
 
 
 class AttnDesc(ctypes.Structure):
@@ -56,6 +56,8 @@ def lib() -> ctypes.CDLL:
         L.csr_prefill_workspace_size.restype = sz
         L.csr_prefill.argtypes = [D, i32, p, p, p, p, p, i32, p, i32, p, i32, i32, p, p, p, sz, p]
         L.csr_prefill.restype = ctypes.c_int
+        L.csr_set_attention_events.argtypes = [p, p]
+        L.csr_set_attention_events.restype = ctypes.c_int
         L.csr_status_string.argtypes = [ctypes.c_int]
         L.csr_status_string.restype = ctypes.c_char_p
         L.csr_last_error.argtypes = []
@@ -74,6 +76,12 @@ def _status_name(st: int) -> str:
 def _check(st: int) -> None:
     if st != CSR_OK:
         raise CsrError(st, lib().csr_last_error().decode())
+
+
+def set_attention_events(begin_event, end_event) -> None:
+    """csr_set_attention_events: raw hipEvent_t handles (ints) or None to disable."""
+    _check(lib().csr_set_attention_events(None if begin_event is None else ctypes.c_void_p(begin_event),
+                                          None if end_event is None else ctypes.c_void_p(end_event)))
 
 
 def make_desc(num_q_heads: int, num_kv_heads: int, head_dim: int, page_size: int = 16, dtype=torch.bfloat16,

@@ -17,6 +17,7 @@
 namespace {
 
 thread_local std::string g_last_error;
+thread_local hipEvent_t g_ev_begin = nullptr, g_ev_end = nullptr;  // csr_set_attention_events
 
 csr_status fail(csr_status st, const char* fmt, ...) __attribute__((format(printf, 2, 3)));
 csr_status fail(csr_status st, const char* fmt, ...) {
@@ -215,8 +216,12 @@ csr_status run_attention(const csr_attn_desc* d, int batch, const void* q, const
   a.nsplit = p.nsplit;
   a.n_units = p.n_units;
   a.xcd_remap = p.xcd_remap;
+  if (g_ev_begin && hipEventRecord(g_ev_begin, stream) != hipSuccess)
+    return fail(CSR_E_HIP, "hipEventRecord(begin) failed");
   st = launched(csr::launch_attention(a, d->dtype == CSR_BF16, stream), "attention");
-  if (st != CSR_OK || p.nsplit == 1) return st;
+  if (st != CSR_OK) return st;
+  if (g_ev_end && hipEventRecord(g_ev_end, stream) != hipSuccess) return fail(CSR_E_HIP, "hipEventRecord(end) failed");
+  if (p.nsplit == 1) return st;
   csr::MergeArgs m;
   m.part_o = a.part_o;
   m.part_lse = a.part_lse;
@@ -245,6 +250,14 @@ const char* csr_status_string(csr_status s) {
 }
 
 const char* csr_last_error(void) { return g_last_error.c_str(); }
+
+csr_status csr_set_attention_events(void* begin_event, void* end_event) {
+  if ((begin_event == nullptr) != (end_event == nullptr))
+    return fail(CSR_E_INVAL, "set both events or neither");
+  g_ev_begin = static_cast<hipEvent_t>(begin_event);
+  g_ev_end = static_cast<hipEvent_t>(end_event);
+  return CSR_OK;
+}
 
 csr_status csr_kv_append(const csr_attn_desc* desc, int32_t batch, const void* k_new, const void* v_new,
                          void* k_pool, void* v_pool, int32_t num_pages, const int32_t* block_table,

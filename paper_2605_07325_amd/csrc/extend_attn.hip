@@ -36,6 +36,8 @@
 //
 // An fp32 instance uses v_mfma_f32_32x32x2f32 with the same layout scheme and
 // never rounds through bf16.
+#include <stdlib.h>
+
 #include "kernels.h"
 
 namespace csr {
@@ -172,14 +174,32 @@ struct TileLoader {
 
 // ---------------------------------------------------------------------------
 // bf16 inputs, fp32 accumulation.
-template <int D, int NB>
-__global__ void __launch_bounds__(NTHREADS, 1) attn_bf16_kernel(AttnArgs a) {
+//
+// K/V tiles move HBM -> LDS with global_load_lds_dwordx4 (no register
+// staging): wave w's j-th instruction fills one 1 KB block of the tile, lane i
+// writing bytes [16i, 16i+16) of it, so each lane fetches the global chunk that
+// the swizzle places in its slot.  Page ids for tile it+1 are loaded while tile
+// it is computed.  Keys at or beyond the tile's last visible key are clamped
+// to it: they are masked for every row of the tile, and a finite value times a
+// zero probability contributes nothing.
+//
+// Online softmax keeps a per-row reference max and rescales O only when a new
+// score exceeds it by more than 2^8 (wave-uniform branch), so the rescale of
+// the fp32 accumulators is rare; probabilities stay below 2^8 and the final
+// normalisation is exact whatever reference was used.
+template <int D, int NB, int NW>
+__global__ void __launch_bounds__(NW * 64, 1) attn_bf16_kernel(const AttnArgs a) {
+  constexpr int NWAVES = NW;
   constexpr int BM = NWAVES * 32 * NB;
   constexpr int ROWB = D * 2;
   constexpr int NCH = ROWB / 16;
   constexpr int DS = D / 16;  // QK^T contraction steps
   constexpr int DB = D / 32;  // 32-wide d blocks of the output
-  __shared__ __attribute__((aligned(16))) char lds[2][2][KT * ROWB];
+  constexpr int TILEB = KT * ROWB;
+  constexpr int ROWS_PER_KB = 1024 / ROWB;
+  constexpr int NDMA = TILEB / (NWAVES * 1024);  // DMA instructions per wave per tensor
+  constexpr float THRESH = 8.f;                  // lazy-rescale threshold (log2 units)
+  __shared__ __attribute__((aligned(1024))) char lds[2 * 2 * TILEB];  // [buf][K|V]
 
   Unit u;
   if (!decode_unit<BM>(a, u)) return;
@@ -189,135 +209,191 @@ __global__ void __launch_bounds__(NTHREADS, 1) attn_bf16_kernel(AttnArgs a) {
   const int l32 = lane & 31;
   const int h = lane >> 5;
   const int G = a.G;
+  const float c = a.scale_log2;
+  const char* __restrict__ kpool = static_cast<const char*>(a.k_pool);
+  const char* __restrict__ vpool = static_cast<const char*>(a.v_pool);
+  const char* __restrict__ knew = static_cast<const char*>(a.k_new);
+  const char* __restrict__ vnew = static_cast<const char*>(a.v_new);
+  const int32_t* __restrict__ bt = a.block_table ? a.block_table + (int64_t)u.b * a.bt_stride : nullptr;
+  const int64_t bt_base = (int64_t)u.b * a.bt_stride;
+  const int log2P = a.log2P, Pmask = (1 << a.log2P) - 1, Hkv = a.Hkv, num_pages = a.num_pages;
 
   // Q^T fragments: lane holds packed row (l32) of each 32-row block, d = ds*16 + 8h .. +7.
   u32x4 qf[NB][DS];
-  int tok[NB];
+  int lim[NB];  // last visible key of the lane's row
   bool valid[NB];
 #pragma unroll
   for (int nb = 0; nb < NB; ++nb) {
     const int m = u.m0 + (wave * NB + nb) * 32 + l32;
     valid[nb] = m < u.rows_total;
-    const int i = m / G, j = m - (m / G) * G;
-    tok[nb] = i;
-    const char* qrow = static_cast<const char*>(a.q) +
-                       (((int64_t)(u.cuq + i) * a.Hq + u.g * G + j) * D + h * 8) * 2;
+    const int i = m / G, j = m - i * G;
+    lim[nb] = u.L + i;
+    const char* qrow = static_cast<const char*>(a.q) + (((int64_t)(u.cuq + i) * a.Hq + u.g * G + j) * D + h * 8) * 2;
 #pragma unroll
     for (int ds = 0; ds < DS; ++ds)
       qf[nb][ds] = valid[nb] ? *reinterpret_cast<const u32x4*>(qrow + ds * 32) : u32x4{0, 0, 0, 0};
   }
-  const int wave_first_tok = (u.m0 + wave * NB * 32) / G;
+  const int wave_first_lim = u.L + (u.m0 + wave * NB * 32) / G;
+
+  // DMA geometry: lane's row within each 1 KB block and its swizzled source chunk.
+  int dma_row[NDMA], dma_chunk[NDMA];
+#pragma unroll
+  for (int j = 0; j < NDMA; ++j) {
+    const int blk = j * NWAVES + wave;
+    dma_row[j] = blk * ROWS_PER_KB + lane / NCH;
+    dma_chunk[j] = (lane % NCH) ^ swz<NCH>(dma_row[j]);
+  }
+  const int last_key = u.kv_end - 1;
+
+  // Byte offset of key row t's chunk for this lane (pool or chunk source).
+  auto row_src = [&](int t, int pg, const char*& kb, const char*& vb) -> int64_t {
+    t = min(t, last_key);
+    if (t < u.L) {
+      if (pg >= 0 && pg < num_pages) {
+        kb = kpool;
+        vb = vpool;
+        return ((((int64_t)pg << log2P) + (t & Pmask)) * Hkv + u.g) * ROWB;
+      }
+      t = u.L;  // invalid page id: never dereferenced, read another valid row instead
+    }
+    kb = knew;
+    vb = vnew;
+    return ((int64_t)(u.cuq + t - u.L) * Hkv + u.g) * ROWB;
+  };
+  auto page_of = [&](int t) -> int {
+    t = min(t, last_key);
+    if (t >= u.L) return 0;
+    const int pidx = t >> log2P;
+    return bt ? __ldg(bt + pidx) : (int)(bt_base + pidx);
+  };
+  auto issue_tile = [&](int tile, const int* pg, int buf) {
+    char* kl = lds + buf * 2 * TILEB;
+    char* vl = kl + TILEB;
+#pragma unroll
+    for (int j = 0; j < NDMA; ++j) {
+      const char* kb;
+      const char* vb;
+      const int64_t off = row_src(tile * KT + dma_row[j], pg[j], kb, vb) + dma_chunk[j] * 16;
+      const int blk = j * NWAVES + wave;
+      __builtin_amdgcn_global_load_lds((const __attribute__((address_space(1))) void*)(kb + off),
+                                       (__attribute__((address_space(3))) void*)(kl + blk * 1024), 16, 0, 0);
+      __builtin_amdgcn_global_load_lds((const __attribute__((address_space(1))) void*)(vb + off),
+                                       (__attribute__((address_space(3))) void*)(vl + blk * 1024), 16, 0, 0);
+    }
+  };
+
+  // Per-lane LDS offsets (buffer and 32-key block offsets are immediates).
+  int koff[DS];
+  {
+    const int sw = swz<NCH>(l32);
+#pragma unroll
+    for (int ds = 0; ds < DS; ++ds) koff[ds] = l32 * ROWB + (((ds * 2 + h) ^ sw) << 4);
+  }
+  const int grp = lane >> 4, rr = (lane & 15) >> 2, qq = lane & 3, hh = grp >> 1;
+  int voff_a[DB], voff_b[DB];
+  {
+    const int ra = 4 * hh + rr, rb = ra + 8;
+#pragma unroll
+    for (int db = 0; db < DB; ++db) {
+      const int dcol = db * 32 + 16 * (grp & 1) + 4 * qq;
+      const int chunk = dcol >> 3, within = (dcol & 7) * 2;
+      voff_a[db] = ra * ROWB + ((chunk ^ swz<NCH>(ra)) << 4) + within;
+      voff_b[db] = rb * ROWB + ((chunk ^ swz<NCH>(rb)) << 4) + within;
+    }
+  }
 
   f32x16 o[NB][DB];
-  float mrow[NB], lrow[NB];
+  float mref[NB], lrow[NB];
 #pragma unroll
   for (int nb = 0; nb < NB; ++nb) {
-    mrow[nb] = -INFINITY;
+    mref[nb] = -INFINITY;
     lrow[nb] = 0.f;
 #pragma unroll
     for (int db = 0; db < DB; ++db) o[nb][db] = f32x16{};
   }
 
-  TileLoader<D, 2> ld;
-  if (u.tb < u.te) {
-    ld.load(a, u, u.tb * KT);
-    ld.store(lds[0][0], lds[0][1]);
-  }
-  __syncthreads();
-
-  // Per-lane constants of the transposing V read: group of 16 lanes, row r within 4, column quad q.
-  const int grp = lane >> 4;
-  const int rr = (lane & 15) >> 2;
-  const int qq = lane & 3;
-  const int hh = grp >> 1;
-
-  for (int it = u.tb; it < u.te; ++it) {
-    const int cur = (it - u.tb) & 1;
-    const bool has_next = it + 1 < u.te;
-    if (has_next) ld.load(a, u, (it + 1) * KT);
-    const char* kl = lds[cur][0];
-    const char* vl = lds[cur][1];
-    const int t0 = it * KT;
-
+  auto compute_tile = [&](const char* kl, int t0, bool masked) {
+    const char* vl = kl + TILEB;
     // S^T = K Q^T for two 32-key blocks.
     f32x16 sacc[NB][2];
 #pragma unroll
     for (int kb = 0; kb < 2; ++kb) {
 #pragma unroll
       for (int nb = 0; nb < NB; ++nb) sacc[nb][kb] = f32x16{};
-      const int row = kb * 32 + l32;
-      const char* kp = kl + row * ROWB;
-      const int sw = swz<NCH>(row);
 #pragma unroll
       for (int ds = 0; ds < DS; ++ds) {
-        const u32x4 kf = *reinterpret_cast<const u32x4*>(kp + (((ds * 2 + h) ^ sw) << 4));
+        const u32x4 kf = *reinterpret_cast<const u32x4*>(kl + kb * 32 * ROWB + koff[ds]);
 #pragma unroll
         for (int nb = 0; nb < NB; ++nb)
           sacc[nb][kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
               __builtin_bit_cast(bf16x8, kf), __builtin_bit_cast(bf16x8, qf[nb][ds]), sacc[nb][kb], 0, 0, 0);
       }
     }
-
-    // Online softmax (log2 domain).
-    const bool need_mask = t0 + KT - 1 > u.L + wave_first_tok;
-    u32x4 pf[NB][4];
+    // Online softmax in the log2 domain with a lazily moved reference max.
+    float mxs[NB];
+    bool grow = false;
 #pragma unroll
     for (int nb = 0; nb < NB; ++nb) {
-      float sv[2][16];
+      if (masked) {
+#pragma unroll
+        for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+          for (int v = 0; v < 16; ++v) {
+            const int t = t0 + kb * 32 + 8 * (v >> 2) + 4 * h + (v & 3);
+            if (t > lim[nb]) sacc[nb][kb][v] = -INFINITY;
+          }
+      }
       float mx = -INFINITY;
 #pragma unroll
       for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
-        for (int v = 0; v < 16; ++v) {
-          float x = sacc[nb][kb][v] * a.scale_log2;
-          if (need_mask) {
-            const int t = t0 + kb * 32 + 8 * (v >> 2) + 4 * h + (v & 3);
-            if (t > u.L + tok[nb]) x = -INFINITY;
-          }
-          sv[kb][v] = x;
-          mx = fmaxf(mx, x);
-        }
+        for (int v = 0; v < 16; v += 2) mx = fmaxf(mx, fmaxf(sacc[nb][kb][v], sacc[nb][kb][v + 1]));
       mx = fmaxf(mx, __shfl_xor(mx, 32));
-      const float m_new = fmaxf(mrow[nb], mx);
-      const float m_use = (m_new == -INFINITY) ? 0.f : m_new;
-      const float alpha = fast_exp2(mrow[nb] - m_use);
+      mxs[nb] = mx * c;
+      grow |= mxs[nb] > mref[nb] + THRESH;
+    }
+    if (__any(grow)) {
+#pragma unroll
+      for (int nb = 0; nb < NB; ++nb) {
+        const float mnew = fmaxf(mref[nb], mxs[nb]);
+        const float alpha = fast_exp2((mref[nb] == -INFINITY ? 0.f : mref[nb]) - (mnew == -INFINITY ? 0.f : mnew));
+        lrow[nb] *= alpha;
+#pragma unroll
+        for (int db = 0; db < DB; ++db) o[nb][db] *= alpha;
+        mref[nb] = mnew;
+      }
+    }
+    u32x4 pf[NB][4];
+#pragma unroll
+    for (int nb = 0; nb < NB; ++nb) {
+      const float neg_m = mref[nb] == -INFINITY ? 0.f : -mref[nb];
+      float p[2][16];
       float rs = 0.f;
 #pragma unroll
       for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
         for (int v = 0; v < 16; ++v) {
-          const float p = fast_exp2(sv[kb][v] - m_use);
-          sv[kb][v] = p;
-          rs += p;
+          p[kb][v] = fast_exp2(__builtin_fmaf(sacc[nb][kb][v], c, neg_m));
+          rs += p[kb][v];
         }
-      rs += __shfl_xor(rs, 32);
-      lrow[nb] = lrow[nb] * alpha + rs;
-      mrow[nb] = m_new;
-#pragma unroll
-      for (int db = 0; db < DB; ++db) o[nb][db] *= alpha;
+      lrow[nb] += rs;
 #pragma unroll
       for (int ks = 0; ks < 4; ++ks) {
         const int kb = ks >> 1, v0 = (ks & 1) * 8;
-        pf[nb][ks] = u32x4{pack_bf16x2(sv[kb][v0 + 0], sv[kb][v0 + 1]), pack_bf16x2(sv[kb][v0 + 2], sv[kb][v0 + 3]),
-                           pack_bf16x2(sv[kb][v0 + 4], sv[kb][v0 + 5]), pack_bf16x2(sv[kb][v0 + 6], sv[kb][v0 + 7])};
+        pf[nb][ks] = u32x4{pack_bf16x2(p[kb][v0 + 0], p[kb][v0 + 1]), pack_bf16x2(p[kb][v0 + 2], p[kb][v0 + 3]),
+                           pack_bf16x2(p[kb][v0 + 4], p[kb][v0 + 5]), pack_bf16x2(p[kb][v0 + 6], p[kb][v0 + 7])};
       }
     }
-
     // O^T += V^T P^T.  Contraction slot 8h+s of step ks is key
     // kb*32 + 16*(ks&1) + 8*(s/4) + 4h + s%4 (kb = ks/2), matching pf.
 #pragma unroll
     for (int ks = 0; ks < 4; ++ks) {
       const int kb = ks >> 1, half = ks & 1;
-      const int row_a = kb * 32 + 16 * half + 4 * hh + rr;
-      const int row_b = row_a + 8;
+      const char* vbase = vl + (kb * 32 + 16 * half) * ROWB;
 #pragma unroll
       for (int db = 0; db < DB; ++db) {
-        const int dcol = db * 32 + 16 * (grp & 1) + 4 * qq;
-        const int chunk = dcol >> 3, within = (dcol & 7) * 2;
-        const char* pa = vl + row_a * ROWB + ((chunk ^ swz<NCH>(row_a)) << 4) + within;
-        const char* pb = vl + row_b * ROWB + ((chunk ^ swz<NCH>(row_b)) << 4) + within;
-        const s16x4 va = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4*)(pa));
-        const s16x4 vb = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4*)(pb));
+        const s16x4 va = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4*)(vbase + voff_a[db]));
+        const s16x4 vb = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4*)(vbase + voff_b[db]));
         const u32x2 wa = __builtin_bit_cast(u32x2, va);
         const u32x2 wb = __builtin_bit_cast(u32x2, vb);
         const u32x4 vf = u32x4{wa[0], wa[1], wb[0], wb[1]};
@@ -327,20 +403,52 @@ __global__ void __launch_bounds__(NTHREADS, 1) attn_bf16_kernel(AttnArgs a) {
               __builtin_bit_cast(bf16x8, vf), __builtin_bit_cast(bf16x8, pf[nb][ks]), o[nb][db], 0, 0, 0);
       }
     }
+  };
 
-    if (has_next) ld.store(lds[cur ^ 1][0], lds[cur ^ 1][1]);
+  // Tiles below first_masked need no causal mask for any row of this wave.
+  int first_masked = (wave_first_lim + 1) / KT;  // first tile containing a key > wave_first_lim
+  first_masked = max(first_masked, u.tb);
+  int pg[NDMA], pg_next[NDMA];
+#pragma unroll
+  for (int j = 0; j < NDMA; ++j) pg_next[j] = 0;
+  if (u.tb < u.te) {
+#pragma unroll
+    for (int j = 0; j < NDMA; ++j) pg[j] = page_of(u.tb * KT + dma_row[j]);
+    issue_tile(u.tb, pg, 0);
+    if (u.tb + 1 < u.te) {
+#pragma unroll
+      for (int j = 0; j < NDMA; ++j) pg[j] = page_of((u.tb + 1) * KT + dma_row[j]);
+    }
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+  }
+  __syncthreads();
+
+  for (int it = u.tb; it < u.te; ++it) {
+    const int cur = (it - u.tb) & 1;
+    if (it + 1 < u.te) {
+      issue_tile(it + 1, pg, cur ^ 1);
+      if (it + 2 < u.te) {
+#pragma unroll
+        for (int j = 0; j < NDMA; ++j) pg_next[j] = page_of((it + 2) * KT + dma_row[j]);
+      }
+    }
+    compute_tile(lds + cur * 2 * TILEB, it * KT, it >= first_masked);
+#pragma unroll
+    for (int j = 0; j < NDMA; ++j) pg[j] = pg_next[j];
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
     __syncthreads();
   }
 
-  // Epilogue: normalise and write o (bf16) and lse, or the split partials.
+  // Epilogue: combine the two half-rows' sums, normalise, write o and lse (or split partials).
 #pragma unroll
   for (int nb = 0; nb < NB; ++nb) {
+    const float lsum = lrow[nb] + __shfl_xor(lrow[nb], 32);
     if (!valid[nb]) continue;
     const int m = u.m0 + (wave * NB + nb) * 32 + l32;
-    const int i = tok[nb], j = m - i * G;
+    const int i = m / G, j = m - i * G;
     const int64_t qrow = (int64_t)(u.cuq + i) * a.Hq + u.g * G + j;
-    const float inv = lrow[nb] > 0.f ? 1.f / lrow[nb] : 0.f;
-    const float lse = lrow[nb] > 0.f ? (mrow[nb] + __log2f(lrow[nb])) * LN2 : -INFINITY;
+    const float inv = lsum > 0.f ? 1.f / lsum : 0.f;
+    const float lse = lsum > 0.f ? (mref[nb] + __log2f(lsum)) * LN2 : -INFINITY;
     if (a.nsplit == 1) {
       char* orow = static_cast<char*>(a.out) + qrow * D * 2;
 #pragma unroll
@@ -514,13 +622,25 @@ __global__ void __launch_bounds__(NTHREADS, 1) attn_f32_kernel(AttnArgs a) {
   }
 }
 
-constexpr int BF16_NB = 2;
+// bf16 launch shapes: 4 waves x 64 rows (one wave per SIMD) or 8 waves x 32
+// rows (two waves per SIMD, so one wave's softmax overlaps the other's MFMAs).
+// Both cover 256 packed rows per workgroup.
+constexpr int BF16_BM = 256;
+
+int bf16_variant() {
+  static int v = -1;
+  if (v < 0) {
+    const char* e = getenv("CSR_ATTN_VARIANT");  // tuning override
+    v = (e && atoi(e) == 0) ? 0 : 1;
+  }
+  return v;
+}
 
 }  // namespace
 
 int attn_block_m(int dtype_bf16, int d) {
   (void)d;
-  return dtype_bf16 ? NWAVES * 32 * BF16_NB : NWAVES * 32;
+  return dtype_bf16 ? BF16_BM : NWAVES * 32;
 }
 
 hipError_t launch_attention(const AttnArgs& a, int dtype_bf16, hipStream_t stream) {
@@ -528,8 +648,13 @@ hipError_t launch_attention(const AttnArgs& a, int dtype_bf16, hipStream_t strea
   unsigned grid = (unsigned)a.n_units;
   if (a.xcd_remap) grid = (grid + 7u) & ~7u;
   if (dtype_bf16) {
-    if (a.d == 128) hipLaunchKernelGGL((attn_bf16_kernel<128, BF16_NB>), dim3(grid), dim3(NTHREADS), 0, stream, a);
-    else hipLaunchKernelGGL((attn_bf16_kernel<64, BF16_NB>), dim3(grid), dim3(NTHREADS), 0, stream, a);
+    if (bf16_variant() == 1) {
+      if (a.d == 128) hipLaunchKernelGGL((attn_bf16_kernel<128, 1, 8>), dim3(grid), dim3(512), 0, stream, a);
+      else hipLaunchKernelGGL((attn_bf16_kernel<64, 1, 8>), dim3(grid), dim3(512), 0, stream, a);
+    } else {
+      if (a.d == 128) hipLaunchKernelGGL((attn_bf16_kernel<128, 2, 4>), dim3(grid), dim3(256), 0, stream, a);
+      else hipLaunchKernelGGL((attn_bf16_kernel<64, 2, 4>), dim3(grid), dim3(256), 0, stream, a);
+    }
   } else {
     if (a.d == 128) hipLaunchKernelGGL((attn_f32_kernel<128>), dim3(grid), dim3(NTHREADS), 0, stream, a);
     else hipLaunchKernelGGL((attn_f32_kernel<64>), dim3(grid), dim3(NTHREADS), 0, stream, a);
