@@ -13,7 +13,8 @@ from typing import Optional
 
 import torch
 
-_LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libcsr.so")
+# CSR_LIBRARY points at an alternative build (A/B tuning); default: the in-tree library.
+_LIB_PATH = os.environ.get("CSR_LIBRARY") or os.path.join(os.path.dirname(os.path.abspath(__file__)), "libcsr.so")
 
 CSR_OK, CSR_E_INVAL, CSR_E_UNSUPPORTED, CSR_E_WORKSPACE, CSR_E_HIP = 0, 1, 2, 3, 4
 CSR_F32, CSR_BF16 = 0, 1

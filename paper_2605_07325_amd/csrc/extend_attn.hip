@@ -38,6 +38,8 @@
 // never rounds through bf16.
 #include <stdlib.h>
 
+#include <type_traits>
+
 #include "kernels.h"
 
 namespace csr {
@@ -54,6 +56,10 @@ typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
 typedef short s16x4 __attribute__((ext_vector_type(4)));
 typedef __attribute__((address_space(3))) s16x4 lds_s16x4;
 
+#ifndef CSR_SCHED
+#define CSR_SCHED 2  // instruction interleaving of the pipelined main loop (0: compiler default)
+#endif
+
 constexpr int KT = 64;        // keys per tile
 constexpr int NTHREADS = 256;  // 4 waves
 constexpr int NWAVES = 4;
@@ -64,6 +70,23 @@ template <int NCH>
 __device__ __forceinline__ int swz(int row) {
   if constexpr (NCH >= 16) return ((row & 7) << 1) | ((row >> 3) & 1);
   else return ((row & 3) << 1) | ((row >> 2) & 1);
+}
+
+// Slot of 16-byte chunk c in key row `row` of an LDS tile: the row XOR plus,
+// for 256-byte rows, a swap of chunk bit 1 into bit 3 so the two 16-lane
+// groups of a transposing V read fall into opposite halves of the 64 banks.
+// A bijection on the chunks of each row; chunk_of_slot is its inverse.
+template <int NCH>
+__device__ __forceinline__ int slot(int row, int c) {
+  int s = c ^ swz<NCH>(row);
+  if constexpr (NCH == 16) s ^= ((c >> 1) & 1) << 3;
+  return s;
+}
+template <int NCH>
+__device__ __forceinline__ int chunk_of_slot(int row, int s) {
+  int c = s ^ swz<NCH>(row);
+  if constexpr (NCH == 16) c ^= ((c >> 1) & 1) << 3;
+  return c;
 }
 
 __device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
@@ -175,36 +198,46 @@ struct TileLoader {
 // ---------------------------------------------------------------------------
 // bf16 inputs, fp32 accumulation.
 //
-// K/V tiles move HBM -> LDS with global_load_lds_dwordx4 (no register
-// staging): wave w's j-th instruction fills one 1 KB block of the tile, lane i
-// writing bytes [16i, 16i+16) of it, so each lane fetches the global chunk that
-// the swizzle places in its slot.  Page ids for tile it+1 are loaded while tile
-// it is computed.  Keys at or beyond the tile's last visible key are clamped
-// to it: they are masked for every row of the tile, and a finite value times a
-// zero probability contributes nothing.
+// One workgroup = 8 waves x 32 packed rows; two waves share each SIMD.
+//
+// K/V tiles (64 keys) move HBM -> LDS with global_load_lds_dwordx4 (no
+// register staging) through 4-stage rings: wave w's j-th DMA instruction fills
+// one 1 KB block of a tile, lane i writing bytes [16i, 16i+16), so each lane
+// fetches the global chunk that lives in its LDS slot.  Tile t is issued three
+// tiles before it is processed; each tile waits only for loads older than the
+// previous tile's.  When a page holds at least the 4 (d=128) or 8 (d=64) keys
+// of one DMA block, the page id is wave-uniform, comes through the scalar
+// cache, and the source address is a scalar base plus a per-lane constant.
+//
+// Main loop (tiles no row of the workgroup needs masked), software-pipelined
+// per 32-key block b inside every wave: the exponentials of block b are
+// computed while the MFMA pipe works on the scores of block b+1, then P(b) V(b)
+// runs while the row maxima of b+1 are reduced.  The loop is unrolled over the
+// ring so every LDS address is a per-lane register plus an immediate.  The
+// diagonal tiles run afterwards, unpipelined, with the causal mask.
 //
 // Online softmax keeps a per-row reference max and rescales O only when a new
-// score exceeds it by more than 2^8 (wave-uniform branch), so the rescale of
-// the fp32 accumulators is rare; probabilities stay below 2^8 and the final
-// normalisation is exact whatever reference was used.
-template <int D, int NB, int NW>
-__global__ void __launch_bounds__(NW * 64, 1) attn_bf16_kernel(const AttnArgs a) {
-  constexpr int NWAVES = NW;
-  constexpr int BM = NWAVES * 32 * NB;
+// score exceeds it by more than 2^8 (wave-uniform branch); probabilities stay
+// below 2^8 and the final normalisation is exact whatever reference was used.
+template <int D, bool SCALAR_PAGES>
+__global__ void __launch_bounds__(512, 1) attn_bf16_kernel(const AttnArgs a) {
+  constexpr int NW = 8;
+  constexpr int BM = NW * 32;
   constexpr int ROWB = D * 2;
   constexpr int NCH = ROWB / 16;
   constexpr int DS = D / 16;  // QK^T contraction steps
   constexpr int DB = D / 32;  // 32-wide d blocks of the output
   constexpr int TILEB = KT * ROWB;
   constexpr int ROWS_PER_KB = 1024 / ROWB;
-  constexpr int NDMA = TILEB / (NWAVES * 1024);  // DMA instructions per wave per tensor
-  constexpr float THRESH = 8.f;                  // lazy-rescale threshold (log2 units)
-  __shared__ __attribute__((aligned(1024))) char lds[2 * 2 * TILEB];  // [buf][K|V]
+  constexpr int NDMA = TILEB / (NW * 1024);  // DMA instructions per wave per tensor tile
+  constexpr int ST = 4;                      // ring stages (K and V each)
+  constexpr float THRESH = 8.f;              // lazy-rescale threshold (log2 units)
+  __shared__ __attribute__((aligned(1024))) char lds[2 * ST * TILEB];
 
   Unit u;
   if (!decode_unit<BM>(a, u)) return;
 
-  const int wave = threadIdx.x >> 6;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int lane = threadIdx.x & 63;
   const int l32 = lane & 31;
   const int h = lane >> 5;
@@ -214,81 +247,88 @@ __global__ void __launch_bounds__(NW * 64, 1) attn_bf16_kernel(const AttnArgs a)
   const char* __restrict__ vpool = static_cast<const char*>(a.v_pool);
   const char* __restrict__ knew = static_cast<const char*>(a.k_new);
   const char* __restrict__ vnew = static_cast<const char*>(a.v_new);
-  const int32_t* __restrict__ bt = a.block_table ? a.block_table + (int64_t)u.b * a.bt_stride : nullptr;
-  const int64_t bt_base = (int64_t)u.b * a.bt_stride;
-  const int log2P = a.log2P, Pmask = (1 << a.log2P) - 1, Hkv = a.Hkv, num_pages = a.num_pages;
-
-  // Q^T fragments: lane holds packed row (l32) of each 32-row block, d = ds*16 + 8h .. +7.
-  u32x4 qf[NB][DS];
-  int lim[NB];  // last visible key of the lane's row
-  bool valid[NB];
-#pragma unroll
-  for (int nb = 0; nb < NB; ++nb) {
-    const int m = u.m0 + (wave * NB + nb) * 32 + l32;
-    valid[nb] = m < u.rows_total;
-    const int i = m / G, j = m - i * G;
-    lim[nb] = u.L + i;
-    const char* qrow = static_cast<const char*>(a.q) + (((int64_t)(u.cuq + i) * a.Hq + u.g * G + j) * D + h * 8) * 2;
-#pragma unroll
-    for (int ds = 0; ds < DS; ++ds)
-      qf[nb][ds] = valid[nb] ? *reinterpret_cast<const u32x4*>(qrow + ds * 32) : u32x4{0, 0, 0, 0};
-  }
-  const int wave_first_lim = u.L + (u.m0 + wave * NB * 32) / G;
-
-  // DMA geometry: lane's row within each 1 KB block and its swizzled source chunk.
-  int dma_row[NDMA], dma_chunk[NDMA];
-#pragma unroll
-  for (int j = 0; j < NDMA; ++j) {
-    const int blk = j * NWAVES + wave;
-    dma_row[j] = blk * ROWS_PER_KB + lane / NCH;
-    dma_chunk[j] = (lane % NCH) ^ swz<NCH>(dma_row[j]);
-  }
+  // The block table is read-only for the kernel's lifetime: reading it through
+  // the constant address space lets wave-uniform lookups use scalar loads,
+  // which the scalar cache serves without queueing behind the K/V DMA.
+  typedef const __attribute__((address_space(4))) int32_t* const_i32p;
+  const_i32p bt = a.block_table ? (const_i32p)(a.block_table + (int64_t)u.b * a.bt_stride) : nullptr;
+  const int bt_base = u.b * a.bt_stride;
+  const int log2P = a.log2P, Pmask = (1 << a.log2P) - 1, num_pages = a.num_pages;
+  const int kv_stride = a.Hkv * ROWB;  // bytes between consecutive tokens of one kv head
   const int last_key = u.kv_end - 1;
 
-  // Byte offset of key row t's chunk for this lane (pool or chunk source).
-  auto row_src = [&](int t, int pg, const char*& kb, const char*& vb) -> int64_t {
-    t = min(t, last_key);
-    if (t < u.L) {
-      if (pg >= 0 && pg < num_pages) {
-        kb = kpool;
-        vb = vpool;
-        return ((((int64_t)pg << log2P) + (t & Pmask)) * Hkv + u.g) * ROWB;
-      }
-      t = u.L;  // invalid page id: never dereferenced, read another valid row instead
-    }
-    kb = knew;
-    vb = vnew;
-    return ((int64_t)(u.cuq + t - u.L) * Hkv + u.g) * ROWB;
-  };
-  auto page_of = [&](int t) -> int {
-    t = min(t, last_key);
+  // Q^T fragment: lane holds packed row (l32), d = ds*16 + 8h .. +7.
+  u32x4 qf[DS];
+  const int m_row = u.m0 + wave * 32 + l32;
+  const bool valid = m_row < u.rows_total;
+  const int tok = m_row / G;
+  const int lim = u.L + tok;  // last key this lane's row sees
+  {
+    const int j = m_row - tok * G;
+    const char* qrow =
+        static_cast<const char*>(a.q) + (((int64_t)(u.cuq + tok) * a.Hq + u.g * G + j) * D + h * 8) * 2;
+#pragma unroll
+    for (int ds = 0; ds < DS; ++ds)
+      qf[ds] = valid ? *reinterpret_cast<const u32x4*>(qrow + ds * 32) : u32x4{0, 0, 0, 0};
+  }
+
+  // ---- DMA: lane's key row within the tile for block j, and its byte offset inside a token row.
+  int drow[NDMA], dchunk[NDMA];
+#pragma unroll
+  for (int j = 0; j < NDMA; ++j) {
+    drow[j] = (j * NW + wave) * ROWS_PER_KB + lane / NCH;
+    dchunk[j] = u.g * ROWB + (chunk_of_slot<NCH>(drow[j], lane % NCH) << 4);
+  }
+  // Page id of DMA block j of `tile` (wave-uniform in scalar mode; unused for chunk keys).
+  auto page_of = [&](int tile, int j) -> int {
+    int t;
+    if constexpr (SCALAR_PAGES)
+      t = min(tile * KT + (j * NW + wave) * ROWS_PER_KB, last_key);
+    else
+      t = min(tile * KT + drow[j], last_key);
     if (t >= u.L) return 0;
     const int pidx = t >> log2P;
-    return bt ? __ldg(bt + pidx) : (int)(bt_base + pidx);
+    return bt ? bt[pidx] : bt_base + pidx;
   };
-  auto issue_tile = [&](int tile, const int* pg, int buf) {
-    char* kl = lds + buf * 2 * TILEB;
-    char* vl = kl + TILEB;
-#pragma unroll
-    for (int j = 0; j < NDMA; ++j) {
-      const char* kb;
-      const char* vb;
-      const int64_t off = row_src(tile * KT + dma_row[j], pg[j], kb, vb) + dma_chunk[j] * 16;
-      const int blk = j * NWAVES + wave;
-      __builtin_amdgcn_global_load_lds((const __attribute__((address_space(1))) void*)(kb + off),
-                                       (__attribute__((address_space(3))) void*)(kl + blk * 1024), 16, 0, 0);
-      __builtin_amdgcn_global_load_lds((const __attribute__((address_space(1))) void*)(vb + off),
-                                       (__attribute__((address_space(3))) void*)(vl + blk * 1024), 16, 0, 0);
+  auto dma = [&](const char* src, char* dst, int j) {
+    __builtin_amdgcn_global_load_lds((const __attribute__((address_space(1))) void*)src,
+                                     (__attribute__((address_space(3))) void*)(dst + (j * NW + wave) * 1024), 16, 0, 0);
+  };
+  // DMA block j of a K or V tile into `dst`.  Pure-prefix and pure-chunk
+  // tiles take a scalar base plus a per-lane constant; a tile straddling L
+  // selects per lane.
+  auto issue_block = [&](int tile, int j, int pgj, char* dst, const char* pool_base, const char* new_base) {
+    const int t0 = tile * KT;
+    const int t_hi = min(t0 + KT - 1, last_key);
+    if (SCALAR_PAGES && t_hi < u.L) {
+      const bool ok = pgj >= 0 && pgj < num_pages;
+      const char* base = ok ? pool_base + (int64_t)pgj * ((int64_t)kv_stride << log2P)
+                            : new_base + (int64_t)u.cuq * kv_stride;  // bad page id: read a valid row instead
+      const int in_page = ok ? (((t0 & Pmask) + drow[j]) & Pmask) : 0;
+      dma(base + in_page * kv_stride + dchunk[j], dst, j);
+    } else if (t0 >= u.L) {
+      const char* base = new_base + (int64_t)(u.cuq + t0 - u.L) * kv_stride;
+      dma(base + min(drow[j], t_hi - t0) * kv_stride + dchunk[j], dst, j);
+    } else {
+      int t = min(t0 + drow[j], last_key);
+      const bool from_pool = t < u.L && pgj >= 0 && pgj < num_pages;
+      if (t < u.L && !from_pool) t = u.L;
+      const int64_t row = from_pool ? ((int64_t)pgj << log2P) + (t & Pmask) : (int64_t)(u.cuq + t - u.L);
+      dma((from_pool ? pool_base : new_base) + row * kv_stride + dchunk[j], dst, j);
     }
   };
-
-  // Per-lane LDS offsets (buffer and 32-key block offsets are immediates).
-  int koff[DS];
-  {
-    const int sw = swz<NCH>(l32);
+  auto issue = [&](int tile, const int* pg, char* dst, const char* pool_base, const char* new_base) {
 #pragma unroll
-    for (int ds = 0; ds < DS; ++ds) koff[ds] = l32 * ROWB + (((ds * 2 + h) ^ sw) << 4);
-  }
+    for (int j = 0; j < NDMA; ++j) issue_block(tile, j, pg[j], dst, pool_base, new_base);
+  };
+  char* const vring = lds;
+  char* const kring = lds + ST * TILEB;
+  const uint32_t lds_addr = (uint32_t)(size_t)((__attribute__((address_space(3))) char*)lds);
+
+  // Per-lane LDS read offsets (stage and 32-key block offsets are added as immediates).
+  int koff[DS];
+#pragma unroll
+  for (int ds = 0; ds < DS; ++ds) koff[ds] = l32 * ROWB + (slot<NCH>(l32, ds * 2 + h) << 4);
   const int grp = lane >> 4, rr = (lane & 15) >> 2, qq = lane & 3, hh = grp >> 1;
   int voff_a[DB], voff_b[DB];
   {
@@ -297,184 +337,271 @@ __global__ void __launch_bounds__(NW * 64, 1) attn_bf16_kernel(const AttnArgs a)
     for (int db = 0; db < DB; ++db) {
       const int dcol = db * 32 + 16 * (grp & 1) + 4 * qq;
       const int chunk = dcol >> 3, within = (dcol & 7) * 2;
-      voff_a[db] = ra * ROWB + ((chunk ^ swz<NCH>(ra)) << 4) + within;
-      voff_b[db] = rb * ROWB + ((chunk ^ swz<NCH>(rb)) << 4) + within;
+      voff_a[db] = ra * ROWB + (slot<NCH>(ra, chunk) << 4) + within;
+      voff_b[db] = rb * ROWB + (slot<NCH>(rb, chunk) << 4) + within;
     }
   }
 
-  f32x16 o[NB][DB];
-  float mref[NB], lrow[NB];
+  f32x16 o[DB];
 #pragma unroll
-  for (int nb = 0; nb < NB; ++nb) {
-    mref[nb] = -INFINITY;
-    lrow[nb] = 0.f;
-#pragma unroll
-    for (int db = 0; db < DB; ++db) o[nb][db] = f32x16{};
-  }
+  for (int db = 0; db < DB; ++db) o[db] = f32x16{};
+  float mref = -INFINITY, lrow = 0.f;
 
-  auto compute_tile = [&](const char* kl, int t0, bool masked) {
-    const char* vl = kl + TILEB;
-    // S^T = K Q^T for two 32-key blocks.
-    f32x16 sacc[NB][2];
+  // Scores of 32-key block kb of a K tile: S^T[key][row] (contraction steps [d0, d1)).
+  auto qk_part = [&](const char* kl, int kb, f32x16& s, int d0, int d1) {
 #pragma unroll
-    for (int kb = 0; kb < 2; ++kb) {
-#pragma unroll
-      for (int nb = 0; nb < NB; ++nb) sacc[nb][kb] = f32x16{};
-#pragma unroll
-      for (int ds = 0; ds < DS; ++ds) {
-        const u32x4 kf = *reinterpret_cast<const u32x4*>(kl + kb * 32 * ROWB + koff[ds]);
-#pragma unroll
-        for (int nb = 0; nb < NB; ++nb)
-          sacc[nb][kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
-              __builtin_bit_cast(bf16x8, kf), __builtin_bit_cast(bf16x8, qf[nb][ds]), sacc[nb][kb], 0, 0, 0);
-      }
+    for (int ds = d0; ds < d1; ++ds) {
+      const u32x4 kf = *reinterpret_cast<const u32x4*>(kl + kb * 32 * ROWB + koff[ds]);
+      s = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, kf), __builtin_bit_cast(bf16x8, qf[ds]),
+                                                  s, 0, 0, 0);
     }
-    // Online softmax in the log2 domain with a lazily moved reference max.
-    float mxs[NB];
-    bool grow = false;
+  };
+  auto qk = [&](const char* kl, int kb, f32x16& s) {
+    s = f32x16{};
 #pragma unroll
-    for (int nb = 0; nb < NB; ++nb) {
-      if (masked) {
-#pragma unroll
-        for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-          for (int v = 0; v < 16; ++v) {
-            const int t = t0 + kb * 32 + 8 * (v >> 2) + 4 * h + (v & 3);
-            if (t > lim[nb]) sacc[nb][kb][v] = -INFINITY;
-          }
-      }
-      float mx = -INFINITY;
-#pragma unroll
-      for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-        for (int v = 0; v < 16; v += 2) mx = fmaxf(mx, fmaxf(sacc[nb][kb][v], sacc[nb][kb][v + 1]));
-      mx = fmaxf(mx, __shfl_xor(mx, 32));
-      mxs[nb] = mx * c;
-      grow |= mxs[nb] > mref[nb] + THRESH;
+    for (int ds = 0; ds < DS; ++ds) {
+      const u32x4 kf = *reinterpret_cast<const u32x4*>(kl + kb * 32 * ROWB + koff[ds]);
+      s = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, kf), __builtin_bit_cast(bf16x8, qf[ds]),
+                                                  s, 0, 0, 0);
     }
-    if (__any(grow)) {
+  };
+  // O^T += V^T P^T for 32-key block kb.  Contraction slot 8h+s of half hf is
+  // key kb*32 + 16*hf + 8*(s/4) + 4h + s%4, matching the probabilities' order.
+  auto pv = [&](const char* vl, int kb, const u32x4* pf) {
 #pragma unroll
-      for (int nb = 0; nb < NB; ++nb) {
-        const float mnew = fmaxf(mref[nb], mxs[nb]);
-        const float alpha = fast_exp2((mref[nb] == -INFINITY ? 0.f : mref[nb]) - (mnew == -INFINITY ? 0.f : mnew));
-        lrow[nb] *= alpha;
-#pragma unroll
-        for (int db = 0; db < DB; ++db) o[nb][db] *= alpha;
-        mref[nb] = mnew;
-      }
-    }
-    u32x4 pf[NB][4];
-#pragma unroll
-    for (int nb = 0; nb < NB; ++nb) {
-      const float neg_m = mref[nb] == -INFINITY ? 0.f : -mref[nb];
-      float p[2][16];
-      float rs = 0.f;
-#pragma unroll
-      for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-        for (int v = 0; v < 16; ++v) {
-          p[kb][v] = fast_exp2(__builtin_fmaf(sacc[nb][kb][v], c, neg_m));
-          rs += p[kb][v];
-        }
-      lrow[nb] += rs;
-#pragma unroll
-      for (int ks = 0; ks < 4; ++ks) {
-        const int kb = ks >> 1, v0 = (ks & 1) * 8;
-        pf[nb][ks] = u32x4{pack_bf16x2(p[kb][v0 + 0], p[kb][v0 + 1]), pack_bf16x2(p[kb][v0 + 2], p[kb][v0 + 3]),
-                           pack_bf16x2(p[kb][v0 + 4], p[kb][v0 + 5]), pack_bf16x2(p[kb][v0 + 6], p[kb][v0 + 7])};
-      }
-    }
-    // O^T += V^T P^T.  Contraction slot 8h+s of step ks is key
-    // kb*32 + 16*(ks&1) + 8*(s/4) + 4h + s%4 (kb = ks/2), matching pf.
-#pragma unroll
-    for (int ks = 0; ks < 4; ++ks) {
-      const int kb = ks >> 1, half = ks & 1;
-      const char* vbase = vl + (kb * 32 + 16 * half) * ROWB;
+    for (int hf = 0; hf < 2; ++hf) {
+      const char* vb = vl + (kb * 32 + 16 * hf) * ROWB;
 #pragma unroll
       for (int db = 0; db < DB; ++db) {
-        const s16x4 va = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4*)(vbase + voff_a[db]));
-        const s16x4 vb = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4*)(vbase + voff_b[db]));
-        const u32x2 wa = __builtin_bit_cast(u32x2, va);
-        const u32x2 wb = __builtin_bit_cast(u32x2, vb);
-        const u32x4 vf = u32x4{wa[0], wa[1], wb[0], wb[1]};
-#pragma unroll
-        for (int nb = 0; nb < NB; ++nb)
-          o[nb][db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
-              __builtin_bit_cast(bf16x8, vf), __builtin_bit_cast(bf16x8, pf[nb][ks]), o[nb][db], 0, 0, 0);
+        const u32x2 wa = __builtin_bit_cast(u32x2, __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4*)(vb + voff_a[db])));
+        const u32x2 wb = __builtin_bit_cast(u32x2, __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4*)(vb + voff_b[db])));
+        o[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, u32x4{wa[0], wa[1], wb[0], wb[1]}),
+                                                        __builtin_bit_cast(bf16x8, pf[hf]), o[db], 0, 0, 0);
       }
     }
   };
-
-  // Tiles below first_masked need no causal mask for any row of this wave.
-  int first_masked = (wave_first_lim + 1) / KT;  // first tile containing a key > wave_first_lim
-  first_masked = max(first_masked, u.tb);
-  int pg[NDMA], pg_next[NDMA];
+  // Same product with the transposing reads issued as inline assembly and a
+  // single explicit LDS wait.  The compiler cannot tell these reads from the
+  // in-flight global->LDS DMA of later tiles and would otherwise wait for all
+  // of that DMA (vmcnt(0)) before each read; the ring protocol already
+  // guarantees the stage was filled (vmcnt + barrier at the tile start).
+  // VOFF is the compile-time LDS byte offset of the 32-key block.
+  auto pv_asm = [&](auto voff_c, const u32x4* pf) {
+    constexpr int VOFF = decltype(voff_c)::value;
+    static_assert(VOFF + 16 * ROWB < 65536, "DS immediate offset range");
+    u32x2 w[2][DB][2];
 #pragma unroll
-  for (int j = 0; j < NDMA; ++j) pg_next[j] = 0;
-  if (u.tb < u.te) {
+    for (int hf = 0; hf < 2; ++hf)
 #pragma unroll
-    for (int j = 0; j < NDMA; ++j) pg[j] = page_of(u.tb * KT + dma_row[j]);
-    issue_tile(u.tb, pg, 0);
-    if (u.tb + 1 < u.te) {
-#pragma unroll
-      for (int j = 0; j < NDMA; ++j) pg[j] = page_of((u.tb + 1) * KT + dma_row[j]);
-    }
-    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
-  }
-  __syncthreads();
-
-  for (int it = u.tb; it < u.te; ++it) {
-    const int cur = (it - u.tb) & 1;
-    if (it + 1 < u.te) {
-      issue_tile(it + 1, pg, cur ^ 1);
-      if (it + 2 < u.te) {
-#pragma unroll
-        for (int j = 0; j < NDMA; ++j) pg_next[j] = page_of((it + 2) * KT + dma_row[j]);
+      for (int db = 0; db < DB; ++db) {
+        asm volatile("ds_read_b64_tr_b16 %0, %1 offset:%2" : "=v"(w[hf][db][0]) : "v"(lds_addr + voff_a[db]), "i"(VOFF + hf * 16 * ROWB));
+        asm volatile("ds_read_b64_tr_b16 %0, %1 offset:%2" : "=v"(w[hf][db][1]) : "v"(lds_addr + voff_b[db]), "i"(VOFF + hf * 16 * ROWB));
       }
+    if constexpr (DB == 4) {
+      asm volatile("s_waitcnt lgkmcnt(0)"
+                   : "+v"(w[0][0][0]), "+v"(w[0][0][1]), "+v"(w[0][1][0]), "+v"(w[0][1][1]), "+v"(w[0][2][0]),
+                     "+v"(w[0][2][1]), "+v"(w[0][3][0]), "+v"(w[0][3][1]), "+v"(w[1][0][0]), "+v"(w[1][0][1]),
+                     "+v"(w[1][1][0]), "+v"(w[1][1][1]), "+v"(w[1][2][0]), "+v"(w[1][2][1]), "+v"(w[1][3][0]),
+                     "+v"(w[1][3][1]));
+    } else {
+      asm volatile("s_waitcnt lgkmcnt(0)"
+                   : "+v"(w[0][0][0]), "+v"(w[0][0][1]), "+v"(w[0][1][0]), "+v"(w[0][1][1]), "+v"(w[1][0][0]),
+                     "+v"(w[1][0][1]), "+v"(w[1][1][0]), "+v"(w[1][1][1]));
     }
-    compute_tile(lds + cur * 2 * TILEB, it * KT, it >= first_masked);
 #pragma unroll
-    for (int j = 0; j < NDMA; ++j) pg[j] = pg_next[j];
+    for (int hf = 0; hf < 2; ++hf)
+#pragma unroll
+      for (int db = 0; db < DB; ++db)
+        o[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
+            __builtin_bit_cast(bf16x8, u32x4{w[hf][db][0][0], w[hf][db][0][1], w[hf][db][1][0], w[hf][db][1][1]}),
+            __builtin_bit_cast(bf16x8, pf[hf]), o[db], 0, 0, 0);
+  };
+  // exp2(s*c - m) packed to bf16 (two contraction halves of 8 keys); adds the row sums.
+  auto softmax_exp = [&](const f32x16& s, u32x4* pf) {
+    const float neg_m = mref == -INFINITY ? 0.f : -mref;
+    float rs = 0.f;
+#pragma unroll
+    for (int hf = 0; hf < 2; ++hf) {
+      float p[8];
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        p[e] = fast_exp2(__builtin_fmaf(s[8 * hf + e], c, neg_m));
+        rs += p[e];
+      }
+      pf[hf] = u32x4{pack_bf16x2(p[0], p[1]), pack_bf16x2(p[2], p[3]), pack_bf16x2(p[4], p[5]),
+                     pack_bf16x2(p[6], p[7])};
+    }
+    lrow += rs;
+  };
+  auto row_max = [&](const f32x16& s) -> float {
+    float mx = fmaxf(s[0], s[1]);
+#pragma unroll
+    for (int v = 2; v < 16; v += 2) mx = fmaxf(mx, fmaxf(s[v], s[v + 1]));
+    const auto pr = __builtin_amdgcn_permlane32_swap(__float_as_uint(mx), __float_as_uint(mx), false, false);
+    return fmaxf(__uint_as_float(pr[0]), __uint_as_float(pr[1])) * c;
+  };
+  // Move the reference max if any row of the wave grew past the threshold.
+  auto update_ref = [&](float mxs) {
+    if (__any(mxs > mref + THRESH)) {
+      const float mnew = fmaxf(mref, mxs);
+      const float alpha = fast_exp2((mref == -INFINITY ? 0.f : mref) - (mnew == -INFINITY ? 0.f : mnew));
+      lrow *= alpha;
+#pragma unroll
+      for (int db = 0; db < DB; ++db) o[db] *= alpha;
+      mref = mnew;
+    }
+  };
+  // One pipelined block step: exponentials of s_cur (block kb of V tile vl)
+  // against the scores of the next block (block kb_next of K tile kl_next).
+  // Each step also issues two DMA blocks (dma_a, dma_b), one after each half
+  // of the score MFMAs, so each wave's loads trickle into the memory pipeline
+  // instead of arriving with every other wave's at the tile boundary.
+  auto step = [&](f32x16& s_cur, f32x16& s_next, auto voff_c, const char* kl_next, int kb_next,
+                  auto dma_a, auto dma_b) {
+    u32x4 pf[2];
+    softmax_exp(s_cur, pf);
+    s_next = f32x16{};
+    qk_part(kl_next, kb_next, s_next, 0, DS / 2);
+    __builtin_amdgcn_sched_barrier(0);
+    dma_a();
+    __builtin_amdgcn_sched_barrier(0);
+    qk_part(kl_next, kb_next, s_next, DS / 2, DS);
+    __builtin_amdgcn_sched_barrier(0);
+    dma_b();
+    __builtin_amdgcn_sched_barrier(0);
+    pv_asm(voff_c, pf);
+    update_ref(row_max(s_next));
+    s_cur = s_next;
+  };
+
+  // ---- main loop: tiles [tb, main_end) are unmasked for every row of the workgroup
+  const int wg_first_lim = u.L + u.m0 / G;
+  const int main_end = max(u.tb, min(u.te, (wg_first_lim + 1) / KT));
+  const int n_main = main_end - u.tb;
+  if (n_main > 0) {
+    // K(tb+k) and V(tb+k) live in stage k % 4.  Every tile issues exactly
+    // 2*NDMA DMA instructions per wave (tiles past the end are clamped to the
+    // last one and land in a stage nobody reads again), so "all but the
+    // previous tile's loads" is the constant vmcnt(2*NDMA).
+    auto clampt = [&](int t) { return min(t, main_end - 1); };
+    int pgn[NDMA];  // pages of tile tb+k+3, issued at tile k
+    {
+      int pg[NDMA];
+#pragma unroll
+      for (int i = 0; i < 3; ++i) {
+#pragma unroll
+        for (int j = 0; j < NDMA; ++j) pg[j] = page_of(clampt(u.tb + i), j);
+        issue(clampt(u.tb + i), pg, kring + i * TILEB, kpool, knew);
+        issue(clampt(u.tb + i), pg, vring + i * TILEB, vpool, vnew);
+      }
+#pragma unroll
+      for (int j = 0; j < NDMA; ++j) pgn[j] = page_of(clampt(u.tb + 3), j);
+    }
     asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+    __syncthreads();
+    f32x16 s_a, s_b;
+    qk(kring, 0, s_a);
+    update_ref(row_max(s_a));
+    // Tile k with ring stage S = k % 4 known at compile time.
+    auto tile = [&](int k, auto stage) {
+      constexpr int S = decltype(stage)::value;
+      // Tiles k and k+1 have landed in LDS (only the previous tile's DMA may
+      // still be in flight) and this wave's LDS reads of tile k-1 are done.
+      // A plain s_barrier: __syncthreads() would also fence, i.e. wait for the
+      // DMA of later tiles too.
+      if constexpr (SCALAR_PAGES) asm volatile("s_waitcnt vmcnt(%0) lgkmcnt(0)" ::"n"(2 * NDMA) : "memory");
+      else asm volatile("s_waitcnt vmcnt(0) lgkmcnt(0)" ::: "memory");
+      __builtin_amdgcn_s_barrier();
+      // K/V(tb+k+3) replace K/V(tb+k-1), last read during tile k-1; their
+      // DMA blocks are spread over the tile's two steps.
+      const int nt = clampt(u.tb + k + 3);
+      char* kdst = kring + ((S + 3) % ST) * TILEB;
+      char* vdst = vring + ((S + 3) % ST) * TILEB;
+      const char* kl = kring + S * TILEB;
+      auto kd0 = [&] { issue_block(nt, 0, pgn[0], kdst, kpool, knew); };
+      auto kd1 = [&] { if constexpr (NDMA > 1) issue_block(nt, NDMA - 1, pgn[NDMA - 1], kdst, kpool, knew); };
+      auto vd0 = [&] { issue_block(nt, 0, pgn[0], vdst, vpool, vnew); };
+      auto vd1 = [&] {
+        if constexpr (NDMA > 1) issue_block(nt, NDMA - 1, pgn[NDMA - 1], vdst, vpool, vnew);
+#pragma unroll
+        for (int j = 0; j < NDMA; ++j) pgn[j] = page_of(clampt(u.tb + k + 4), j);
+      };
+      // block 0 || scores of block 1, then block 1 || scores of the next tile's block 0
+      step(s_a, s_b, std::integral_constant<int, S * TILEB>{}, kl, 1, kd0, kd1);
+      step(s_a, s_b, std::integral_constant<int, S * TILEB + 32 * ROWB>{}, kring + ((S + 1) % ST) * TILEB, 0, vd0, vd1);
+    };
+    for (int k = 0; k < n_main; k += 4) {
+      tile(k, std::integral_constant<int, 0>{});
+      if (k + 1 >= n_main) break;
+      tile(k + 1, std::integral_constant<int, 1>{});
+      if (k + 2 >= n_main) break;
+      tile(k + 2, std::integral_constant<int, 2>{});
+      if (k + 3 >= n_main) break;
+      tile(k + 3, std::integral_constant<int, 3>{});
+    }
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+    __syncthreads();  // every wave is done with the rings before the tail reuses them
+  }
+
+  // ---- tail: tiles [main_end, te) with the causal mask, one tile at a time
+  for (int it = max(main_end, u.tb); it < u.te; ++it) {
+    int pg[NDMA];
+#pragma unroll
+    for (int j = 0; j < NDMA; ++j) pg[j] = page_of(it, j);
+    issue(it, pg, kring, kpool, knew);
+    issue(it, pg, vring, vpool, vnew);
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+    __syncthreads();
+    const int t0 = it * KT;
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb) {
+      f32x16 s;
+      qk(kring, kb, s);
+      if (t0 + kb * 32 + 31 > lim) {
+#pragma unroll
+        for (int v = 0; v < 16; ++v)
+          if (t0 + kb * 32 + 8 * (v >> 2) + 4 * h + (v & 3) > lim) s[v] = -INFINITY;
+      }
+      update_ref(row_max(s));
+      u32x4 pf[2];
+      softmax_exp(s, pf);
+      pv(vring, kb, pf);
+    }
     __syncthreads();
   }
 
   // Epilogue: combine the two half-rows' sums, normalise, write o and lse (or split partials).
+  const auto pr = __builtin_amdgcn_permlane32_swap(__float_as_uint(lrow), __float_as_uint(lrow), false, false);
+  const float lsum = __uint_as_float(pr[0]) + __uint_as_float(pr[1]);
+  if (!valid) return;
+  const int64_t qrow = (int64_t)(u.cuq + tok) * a.Hq + u.g * G + (m_row - tok * G);
+  const float inv = lsum > 0.f ? 1.f / lsum : 0.f;
+  const float lse = lsum > 0.f ? (mref + __log2f(lsum)) * LN2 : -INFINITY;
+  if (a.nsplit == 1) {
+    char* orow = static_cast<char*>(a.out) + qrow * D * 2;
 #pragma unroll
-  for (int nb = 0; nb < NB; ++nb) {
-    const float lsum = lrow[nb] + __shfl_xor(lrow[nb], 32);
-    if (!valid[nb]) continue;
-    const int m = u.m0 + (wave * NB + nb) * 32 + l32;
-    const int i = m / G, j = m - i * G;
-    const int64_t qrow = (int64_t)(u.cuq + i) * a.Hq + u.g * G + j;
-    const float inv = lsum > 0.f ? 1.f / lsum : 0.f;
-    const float lse = lsum > 0.f ? (mref[nb] + __log2f(lsum)) * LN2 : -INFINITY;
-    if (a.nsplit == 1) {
-      char* orow = static_cast<char*>(a.out) + qrow * D * 2;
+    for (int db = 0; db < DB; ++db)
 #pragma unroll
-      for (int db = 0; db < DB; ++db)
+      for (int vg = 0; vg < 4; ++vg) {
+        const int d0 = db * 32 + 8 * vg + 4 * h;
+        const u32x2 w = {pack_bf16x2(o[db][4 * vg + 0] * inv, o[db][4 * vg + 1] * inv),
+                         pack_bf16x2(o[db][4 * vg + 2] * inv, o[db][4 * vg + 3] * inv)};
+        *reinterpret_cast<u32x2*>(orow + d0 * 2) = w;
+      }
+    if (h == 0 && a.lse) a.lse[qrow] = lse;
+  } else {
+    const int64_t prow = (int64_t)u.s * a.total_q * a.Hq + qrow;
+    float* orow = a.part_o + prow * D;
 #pragma unroll
-        for (int vg = 0; vg < 4; ++vg) {
-          const int d0 = db * 32 + 8 * vg + 4 * h;
-          const u32x2 w = {pack_bf16x2(o[nb][db][4 * vg + 0] * inv, o[nb][db][4 * vg + 1] * inv),
-                           pack_bf16x2(o[nb][db][4 * vg + 2] * inv, o[nb][db][4 * vg + 3] * inv)};
-          *reinterpret_cast<u32x2*>(orow + d0 * 2) = w;
-        }
-      if (h == 0 && a.lse) a.lse[qrow] = lse;
-    } else {
-      const int64_t prow = (int64_t)u.s * a.total_q * a.Hq + qrow;
-      float* orow = a.part_o + prow * D;
+    for (int db = 0; db < DB; ++db)
 #pragma unroll
-      for (int db = 0; db < DB; ++db)
-#pragma unroll
-        for (int vg = 0; vg < 4; ++vg) {
-          const int d0 = db * 32 + 8 * vg + 4 * h;
-          const f32x4 w = {o[nb][db][4 * vg + 0] * inv, o[nb][db][4 * vg + 1] * inv, o[nb][db][4 * vg + 2] * inv,
-                           o[nb][db][4 * vg + 3] * inv};
-          *reinterpret_cast<f32x4*>(orow + d0) = w;
-        }
-      if (h == 0) a.part_lse[prow] = lse;
-    }
+      for (int vg = 0; vg < 4; ++vg) {
+        const int d0 = db * 32 + 8 * vg + 4 * h;
+        const f32x4 w = {o[db][4 * vg + 0] * inv, o[db][4 * vg + 1] * inv, o[db][4 * vg + 2] * inv,
+                         o[db][4 * vg + 3] * inv};
+        *reinterpret_cast<f32x4*>(orow + d0) = w;
+      }
+    if (h == 0) a.part_lse[prow] = lse;
   }
 }
 
@@ -622,19 +749,7 @@ __global__ void __launch_bounds__(NTHREADS, 1) attn_f32_kernel(AttnArgs a) {
   }
 }
 
-// bf16 launch shapes: 4 waves x 64 rows (one wave per SIMD) or 8 waves x 32
-// rows (two waves per SIMD, so one wave's softmax overlaps the other's MFMAs).
-// Both cover 256 packed rows per workgroup.
-constexpr int BF16_BM = 256;
-
-int bf16_variant() {
-  static int v = -1;
-  if (v < 0) {
-    const char* e = getenv("CSR_ATTN_VARIANT");  // tuning override
-    v = (e && atoi(e) == 0) ? 0 : 1;
-  }
-  return v;
-}
+constexpr int BF16_BM = 256;  // 8 waves x 32 packed rows
 
 }  // namespace
 
@@ -648,12 +763,14 @@ hipError_t launch_attention(const AttnArgs& a, int dtype_bf16, hipStream_t strea
   unsigned grid = (unsigned)a.n_units;
   if (a.xcd_remap) grid = (grid + 7u) & ~7u;
   if (dtype_bf16) {
-    if (bf16_variant() == 1) {
-      if (a.d == 128) hipLaunchKernelGGL((attn_bf16_kernel<128, 1, 8>), dim3(grid), dim3(512), 0, stream, a);
-      else hipLaunchKernelGGL((attn_bf16_kernel<64, 1, 8>), dim3(grid), dim3(512), 0, stream, a);
+    // Scalar page-id loads need every DMA block (4 keys at d=128, 8 at d=64) inside one page.
+    const bool scalar_pages = a.P >= (a.d == 128 ? 4 : 8);
+    if (a.d == 128) {
+      if (scalar_pages) hipLaunchKernelGGL((attn_bf16_kernel<128, true>), dim3(grid), dim3(512), 0, stream, a);
+      else hipLaunchKernelGGL((attn_bf16_kernel<128, false>), dim3(grid), dim3(512), 0, stream, a);
     } else {
-      if (a.d == 128) hipLaunchKernelGGL((attn_bf16_kernel<128, 2, 4>), dim3(grid), dim3(256), 0, stream, a);
-      else hipLaunchKernelGGL((attn_bf16_kernel<64, 2, 4>), dim3(grid), dim3(256), 0, stream, a);
+      if (scalar_pages) hipLaunchKernelGGL((attn_bf16_kernel<64, true>), dim3(grid), dim3(512), 0, stream, a);
+      else hipLaunchKernelGGL((attn_bf16_kernel<64, false>), dim3(grid), dim3(512), 0, stream, a);
     }
   } else {
     if (a.d == 128) hipLaunchKernelGGL((attn_f32_kernel<128>), dim3(grid), dim3(NTHREADS), 0, stream, a);
