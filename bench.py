@@ -8,7 +8,8 @@ CSR_APPEND).  The default workload is one layer with a 122880-token cached
 prefix and a 512-token chunk, GQA 64 query / 4 kv heads, head_dim 128, bf16,
 page size 16.
 
-Timing: W untimed warm-up steps, then exactly K steps between two
+Timing: W untimed warm-up steps (the GPU clock ramps over the first ~10
+calls), then exactly K steps between two
 synchronisations, timed with events on the stream the library launches on.
 Consecutive steps read different copies of the K/V pool (three copies of about
 250 MB), so the 256 MB Infinity Cache cannot serve a step's prefix from the
@@ -126,8 +127,8 @@ def cpu_baseline(case, target_s: float):
 def main():
     ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=20)
-    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--steps", type=int, default=30)
+    ap.add_argument("--warmup", type=int, default=10)
     ap.add_argument("--workload", default="c3_512",
                     help="c3_<n> extend over a 122880 prefix (default n=512), c2, c5, c1, c4_<S> (prefill)")
     ap.add_argument("--pools", type=int, default=3, help="K/V pool copies rotated across steps")

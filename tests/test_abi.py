@@ -1,0 +1,145 @@
+"""C-ABI checks that need no GPU: the library loads, exports every function
+include/csr.h declares, and rejects malformed arguments on the host before
+any HIP runtime call (no argument below would be valid on a device either)."""
+import ctypes
+import os
+import re
+
+import pytest
+
+from paper_2605_07325_amd import csr
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "csr.h")
+
+FAKE = 0x100000  # 16-byte aligned, never dereferenced: validation fails first
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(csr_[a-z_]+)\s*\(", text)))
+
+
+def test_library_exports_every_declared_function():
+    lib = csr.lib()
+    names = declared_functions()
+    assert set(names) == set(csr.EXPORTS)
+    for name in names:
+        assert hasattr(lib, name), name
+
+
+def test_status_strings():
+    lib = csr.lib()
+    for code, name in [(0, "CSR_OK"), (1, "CSR_E_INVAL"), (2, "CSR_E_UNSUPPORTED"), (3, "CSR_E_WORKSPACE"),
+                       (4, "CSR_E_HIP")]:
+        assert lib.csr_status_string(code).decode() == name
+    assert lib.csr_status_string(99).decode() == "CSR_E_UNKNOWN"
+
+
+def call_extend(desc, batch=1, q=FAKE, kn=FAKE, vn=FAKE, kp=FAKE, vp=FAKE, num_pages=64, bt=FAKE, bt_stride=8,
+                cu=FAKE, cl=FAKE, total_q=16, max_q=16, max_l=100, flags=0, out=FAKE, lse=None, ws=None, ws_bytes=0):
+    lib = csr.lib()
+    p = lambda x: None if x is None else ctypes.c_void_p(x)  # noqa: E731
+    return lib.csr_extend_attention(None if desc is None else ctypes.byref(desc), batch, p(q), p(kn), p(vn), p(kp),
+                                    p(vp), num_pages, p(bt), bt_stride, p(cu), p(cl), total_q, max_q, max_l, flags,
+                                    p(out), p(lse), p(ws), ws_bytes, None)
+
+
+def good_desc(**over):
+    kw = dict(num_q_heads=16, num_kv_heads=2, head_dim=128, page_size=16)
+    kw.update(over)
+    return csr.make_desc(**kw)
+
+
+@pytest.mark.parametrize("desc,code", [
+    (None, csr.CSR_E_INVAL),
+    (csr.AttnDesc(16, 3, 128, 16, 0.0, csr.CSR_BF16), csr.CSR_E_INVAL),   # Hq % Hkv
+    (csr.AttnDesc(0, 1, 128, 16, 0.0, csr.CSR_BF16), csr.CSR_E_INVAL),    # no heads
+    (csr.AttnDesc(16, 2, 96, 16, 0.0, csr.CSR_BF16), csr.CSR_E_UNSUPPORTED),  # head_dim
+    (csr.AttnDesc(16, 2, 128, 16, 0.0, 7), csr.CSR_E_UNSUPPORTED),        # dtype
+    (csr.AttnDesc(16, 2, 128, 12, 0.0, csr.CSR_BF16), csr.CSR_E_INVAL),   # page size not a power of two
+    (csr.AttnDesc(16, 2, 128, 2048, 0.0, csr.CSR_BF16), csr.CSR_E_INVAL),  # page size too large
+    (csr.AttnDesc(16, 2, 128, 16, -1.0, csr.CSR_BF16), csr.CSR_E_INVAL),  # negative scale
+    (csr.AttnDesc(16, 2, 128, 16, float("nan"), csr.CSR_BF16), csr.CSR_E_INVAL),
+])
+def test_descriptor_validation(desc, code):
+    assert call_extend(desc) == code
+    assert csr.lib().csr_last_error().decode()
+
+
+@pytest.mark.parametrize("over,code", [
+    (dict(q=FAKE + 8), csr.CSR_E_INVAL),           # misaligned q
+    (dict(out=None), csr.CSR_E_INVAL),             # no output
+    (dict(cu=None), csr.CSR_E_INVAL),              # no cu_seqlens
+    (dict(kp=None), csr.CSR_E_INVAL),              # prefix but no pool
+    (dict(cl=None), csr.CSR_E_INVAL),              # prefix lengths missing
+    (dict(max_q=17), csr.CSR_E_INVAL),             # max_seqlen_q > total_q
+    (dict(max_q=0), csr.CSR_E_INVAL),
+    (dict(batch=-1), csr.CSR_E_INVAL),
+    (dict(bt_stride=0), csr.CSR_E_INVAL),
+    (dict(bt_stride=4), csr.CSR_E_INVAL),          # 4 pages of 16 cannot hold 100 cached positions
+    (dict(num_pages=0), csr.CSR_E_INVAL),
+    (dict(flags=2), csr.CSR_E_INVAL),              # unknown flag
+    (dict(lse=FAKE + 2), csr.CSR_E_INVAL),         # misaligned lse
+    (dict(batch=0, total_q=3), csr.CSR_E_INVAL),
+])
+def test_argument_validation(over, code):
+    assert call_extend(good_desc(), **over) == code
+
+
+def test_empty_call_is_a_noop():
+    assert call_extend(good_desc(), total_q=0, max_q=0) == csr.CSR_OK
+
+
+def test_missing_workspace_is_reported():
+    desc = good_desc(num_q_heads=64, num_kv_heads=4)
+    need = csr.extend_workspace_size(desc, 1, 512, 512, 122880)
+    assert need > 0  # 120K prefix with a 512-token chunk splits the key range
+    st = call_extend(desc, total_q=512, max_q=512, max_l=122880, bt_stride=7712, num_pages=7712, ws=None)
+    assert st == csr.CSR_E_WORKSPACE
+    st = call_extend(desc, total_q=512, max_q=512, max_l=122880, bt_stride=7712, num_pages=7712, ws=FAKE,
+                     ws_bytes=need - 16)
+    assert st == csr.CSR_E_WORKSPACE
+
+
+def test_workspace_query_rejects_bad_sizes():
+    d = good_desc()
+    assert csr.extend_workspace_size(d, 0, 16, 16, 100) == 0
+    assert csr.extend_workspace_size(csr.AttnDesc(16, 3, 128, 16, 0.0, csr.CSR_BF16), 1, 16, 16, 100) == 0
+
+
+def test_kv_append_validation():
+    lib = csr.lib()
+    p = ctypes.c_void_p
+    d = good_desc()
+    args = lambda **o: dict(dict(batch=1, kn=FAKE, vn=FAKE, kp=FAKE, vp=FAKE, pages=8, bt=FAKE, bts=4, cu=FAKE,  # noqa: E731
+                                 cl=FAKE, total=8), **o)
+    def run(**o):
+        a = args(**o)
+        return lib.csr_kv_append(ctypes.byref(d), a["batch"], p(a["kn"]) if a["kn"] else None, p(a["vn"]) if a["vn"] else None,
+                                 p(a["kp"]) if a["kp"] else None, p(a["vp"]) if a["vp"] else None, a["pages"],
+                                 p(a["bt"]), a["bts"], p(a["cu"]) if a["cu"] else None, p(a["cl"]), a["total"], None)
+    assert run(kp=None) == csr.CSR_E_INVAL
+    assert run(kn=FAKE + 4) == csr.CSR_E_INVAL
+    assert run(pages=0) == csr.CSR_E_INVAL
+    assert run(cu=None) == csr.CSR_E_INVAL
+    assert run(total=0) == csr.CSR_OK
+
+
+def test_prefill_validation():
+    lib = csr.lib()
+    p = ctypes.c_void_p
+    d = good_desc()
+    # max_seqlen above total
+    assert lib.csr_prefill(ctypes.byref(d), 1, p(FAKE), p(FAKE), p(FAKE), None, None, 0, None, 1, p(FAKE), 8, 9,
+                           p(FAKE), None, None, 0, None) == csr.CSR_E_INVAL
+    # only one pool given
+    assert lib.csr_prefill(ctypes.byref(d), 1, p(FAKE), p(FAKE), p(FAKE), p(FAKE), None, 4, None, 1, p(FAKE), 8, 8,
+                           p(FAKE), None, None, 0, None) == csr.CSR_E_INVAL
+
+
+def test_event_hook_requires_both_events():
+    lib = csr.lib()
+    assert lib.csr_set_attention_events(ctypes.c_void_p(FAKE), None) == csr.CSR_E_INVAL
+    assert lib.csr_set_attention_events(None, None) == csr.CSR_OK

@@ -1,0 +1,216 @@
+"""GPU checks built on constructed inputs and the paper's invariants.
+
+At long prefixes random-data parity cannot see a dropped or misplaced page
+(attention is nearly uniform), so these tests construct inputs whose answer
+depends on exactly which cache row is read: a needle key per row, and a
+position-encoding value channel.  They also check the prefix-stability and
+append-only invariants end to end on the device, determinism, and ragged
+batches with empty chunks.
+"""
+import math
+
+import numpy as np
+import pytest
+import torch
+
+from oracle import oracle
+from paper_2605_07325_amd import csr
+from paper_2605_07325_amd import datagen as dg
+from tests.gpu_harness import Dev, compare, from_dev, note, oracle_rows, values
+
+pytestmark = pytest.mark.gpu
+
+
+def slot_of(case, b, t):
+    """Pool (page, in-page index) of cached position t of sequence b."""
+    page = case.block_table[b, t // case.page_size] if case.block_table is not None else b * case.bt_stride + t // case.page_size
+    return int(page), t % case.page_size
+
+
+def test_needle_in_page_selects_the_right_cache_row():
+    """Each checked row i gets a needle key t*(i) in its own page: K[t*] = Q_i =
+    alpha*u_i (a bf16 unit vector scaled so the needle's score is ~60 above the
+    rest).  Output row i must then equal V[t*] to bf16 precision, so reading any
+    other page or slot shows up as an O(1) error."""
+    case = dg.make_case("needle", dtype=dg.BF16, num_q_heads=16, num_kv_heads=1, head_dim=128, cache_len=[8192],
+                        seqlen_q=[64], page_size=16, scale=0.5, seed=5, cfg_id=400)
+    g = np.random.default_rng(11)
+    rows = np.arange(0, 64, 4)  # chunk rows 0, 4, ..., 60 (head 0 of each)
+    pages = g.choice(8192 // 16, size=len(rows), replace=False)
+    alpha = math.sqrt(60 * math.sqrt(128))
+    targets = []
+    for r, pg in zip(rows, pages):
+        t = int(pg) * 16 + int(g.integers(16))
+        u = g.standard_normal(128)
+        u /= np.linalg.norm(u)
+        vec = dg.to_bf16_bits((alpha * u).astype(np.float32))
+        page, s = slot_of(case, 0, t)
+        case.k_pool[page, s, 0] = vec
+        case.q[r, 0] = vec
+        targets.append((r, page, s))
+    note("needle: 16 needles in distinct pages of an 8192-token prefix")
+    dev = Dev(case)
+    out, lse = dev.extend()
+    torch.cuda.synchronize()
+    got = values(case, out)
+    for r, page, s in targets:
+        want = dg.bf16_bits_to_f32(case.v_pool[page, s, 0]).astype(np.float64)
+        assert np.abs(got[r, 0] - want).max() < 2e-2, (r, page, s)
+    ref, ref_lse = oracle_rows(case, rows.astype(np.int32))
+    compare(case, out, lse, rows.astype(np.int32), ref, ref_lse, "needle")
+
+
+def test_position_probe_sees_exactly_the_visible_keys():
+    """K == 0 makes every score 0, so o_i = mean of V over keys 0..L+i.  With
+    V[t, :] = (t mod 251)/256 (exact in bf16) the result is a closed form; a
+    missing, duplicated or reordered page changes the mean."""
+    L, n = 2000, 40
+    case = dg.make_case("probe", dtype=dg.BF16, num_q_heads=8, num_kv_heads=2, head_dim=128, cache_len=[L],
+                        seqlen_q=[n], page_size=16, scale=0.5, seed=6, cfg_id=401, keep_prefix=True)
+    zero = np.uint16(0)
+    case.k_new[:] = zero
+    case.k_pool[:] = zero
+    val = lambda t: dg.to_bf16_bits(np.full(128, (t % 251) / 256.0, np.float32))  # noqa: E731
+    for t in range(L):
+        page, s = slot_of(case, 0, t)
+        case.v_pool[page, s, :] = val(t)
+    for i in range(n):
+        case.v_new[i, :] = val(L + i)
+    note("position probe: L=2000 n=40")
+    dev = Dev(case)
+    out, lse = dev.extend()
+    torch.cuda.synchronize()
+    got = values(case, out)
+    got_lse = lse.cpu().numpy()
+    for i in range(n):
+        expect = np.mean([(t % 251) / 256.0 for t in range(L + i + 1)])
+        assert np.abs(got[i] - expect).max() < 4e-3, i
+        assert abs(got_lse[i, 0] - math.log(L + i + 1)) < 1e-4
+    rows = np.arange(n, dtype=np.int32)
+    ref, ref_lse = oracle_rows(case, rows)
+    compare(case, out, lse, rows, ref, ref_lse, "probe")
+
+
+def test_prefix_stability_extend_equals_prefill_tail_on_gpu():
+    """Cached K/V are not altered by later tokens: extend over an L-token cache
+    equals the last n rows of a full re-prefill over the same L+n tokens (here
+    both computed by the library, then both against the oracle)."""
+    L, n = 6000, 300
+    case = dg.make_case("stab", dtype=dg.BF16, num_q_heads=64, num_kv_heads=4, head_dim=128, cache_len=[L],
+                        seqlen_q=[n], page_size=16, scale=0.5, seed=7, cfg_id=402, keep_prefix=True)
+    full = dg.make_case("stab_full", dtype=dg.BF16, num_q_heads=64, num_kv_heads=4, head_dim=128, cache_len=[0],
+                        seqlen_q=[L + n], page_size=16, scale=0.5, seed=8, cfg_id=403)
+    full.k_new[:] = np.concatenate([case.k_prefix[0], case.k_new])
+    full.v_new[:] = np.concatenate([case.v_prefix[0], case.v_new])
+    full.q[L:] = case.q
+    note("prefix stability: extend L=6000 n=300 vs prefill 6300")
+    out_e, lse_e = Dev(case).extend()
+    out_p, lse_p = Dev(full).prefill(write_cache=False)
+    torch.cuda.synchronize()
+    tail = values(full, out_p)[L:]
+    head = values(case, out_e)
+    assert np.abs(tail - head).max() < 1e-2
+    assert np.abs(lse_p.cpu().numpy()[L:] - lse_e.cpu().numpy()).max() < 1e-4
+    rows = dg.sample_rows(case, 48, cfg_id=402)
+    ref, ref_lse = oracle_rows(case, rows)
+    compare(case, out_e, lse_e, rows, ref, ref_lse, "stab/extend")
+    compare(full, out_p[L:], lse_p[L:], rows, ref, ref_lse, "stab/prefill-tail")
+
+
+def test_append_then_extend_equals_one_shot_extend():
+    """Incremental extensibility: extend chunk A (n1 tokens) with append, then
+    extend chunk B over the longer cache; B's rows equal those of one extend
+    over A+B, and the pool equals the oracle's appends bit for bit."""
+    L, n1, n2 = 3000, 200, 150
+    one = dg.make_case("ab", dtype=dg.BF16, num_q_heads=32, num_kv_heads=2, head_dim=128, cache_len=[L],
+                       seqlen_q=[n1 + n2], page_size=16, scale=0.5, seed=9, cfg_id=404)
+    note("chunk split: L=3000 n1=200 n2=150")
+    out_one, lse_one = Dev(one).extend()
+    # split: first chunk = first n1 tokens, appended; second chunk attends over L + n1 cached tokens
+    a = dg.make_case("a", dtype=dg.BF16, num_q_heads=32, num_kv_heads=2, head_dim=128, cache_len=[L],
+                     seqlen_q=[n1], page_size=16, scale=0.5, seed=9, cfg_id=404)
+    a.q[:] = one.q[:n1]
+    a.k_new[:] = one.k_new[:n1]
+    a.v_new[:] = one.v_new[:n1]
+    a.k_pool, a.v_pool, a.block_table, a.bt_stride = one.k_pool.copy(), one.v_pool.copy(), one.block_table, one.bt_stride
+    dev_a = Dev(a)
+    out_a, _ = dev_a.extend(append=True)
+    b = dg.make_case("b", dtype=dg.BF16, num_q_heads=32, num_kv_heads=2, head_dim=128, cache_len=[L + n1],
+                     seqlen_q=[n2], page_size=16, scale=0.5, seed=9, cfg_id=404)
+    b.q[:] = one.q[n1:]
+    b.k_new[:] = one.k_new[n1:]
+    b.v_new[:] = one.v_new[n1:]
+    b.block_table, b.bt_stride = one.block_table, one.bt_stride
+    dev_b = Dev(b)
+    dev_b.k_pool, dev_b.v_pool = dev_a.k_pool, dev_a.v_pool  # the pool after A's append
+    out_b, lse_b = dev_b.extend()
+    torch.cuda.synchronize()
+    assert np.abs(values(b, out_b) - values(one, out_one)[n1:]).max() < 1e-2
+    assert np.abs(values(a, out_a) - values(one, out_one)[:n1]).max() < 1e-2
+    assert np.abs(lse_b.cpu().numpy() - lse_one.cpu().numpy()[n1:]).max() < 1e-4
+    kp, vp = oracle.kv_append(a.k_new, a.v_new, one.k_pool, one.v_pool, one.block_table, one.bt_stride,
+                              a.cu_seqlens_q, a.cache_len, 2, 128, 16)
+    np.testing.assert_array_equal(from_dev(a, dev_a.k_pool), kp)
+    np.testing.assert_array_equal(from_dev(a, dev_a.v_pool), vp)
+
+
+@pytest.mark.parametrize("cfg", ["c2", "c5"])
+def test_deterministic(cfg):
+    case = dg.config(cfg)
+    note(f"determinism {cfg}")
+    dev = Dev(case)
+    o1, l1 = dev.extend()
+    o2, l2 = dev.extend()
+    torch.cuda.synchronize()
+    assert torch.equal(o1.view(torch.int16), o2.view(torch.int16))
+    assert torch.equal(l1, l2)
+
+
+def test_ragged_batch_with_empty_chunks():
+    case = dg.make_case("empty", dtype=dg.BF16, num_q_heads=16, num_kv_heads=2, head_dim=128,
+                        cache_len=[500, 700, 0, 1200, 64], seqlen_q=[33, 0, 20, 0, 7], page_size=16, scale=0.5,
+                        seed=10, cfg_id=405, interleave=True)
+    note("ragged batch with empty chunks")
+    dev = Dev(case)
+    out, lse = dev.extend(append=True)
+    torch.cuda.synchronize()
+    rows = np.arange(case.total_q, dtype=np.int32)
+    ref, ref_lse = oracle_rows(case, rows)
+    compare(case, out, lse, rows, ref, ref_lse, "empty-chunks")
+    kp, vp = oracle.kv_append(case.k_new, case.v_new, case.k_pool, case.v_pool, case.block_table, case.bt_stride,
+                              case.cu_seqlens_q, case.cache_len, 2, 128, 16)
+    np.testing.assert_array_equal(from_dev(case, dev.k_pool), kp)
+    np.testing.assert_array_equal(from_dev(case, dev.v_pool), vp)
+
+
+def test_custom_softmax_scale_and_prefill_cache_write_small_pages():
+    case = dg.make_case("scale", dtype=dg.BF16, num_q_heads=8, num_kv_heads=8, head_dim=64, cache_len=[0],
+                        seqlen_q=[333], page_size=2, scale=0.5, seed=12, cfg_id=406)
+    note("prefill with scale 0.2, page size 2, d=64, MHA")
+    dev = Dev(case)
+    dev.desc.softmax_scale = 0.2
+    out, lse = dev.prefill(write_cache=True)
+    torch.cuda.synchronize()
+    rows = np.arange(case.total_q, dtype=np.int32)
+    ref, ref_lse, _ = oracle.attention(oracle.BF16, case.q, case.k_new, case.v_new, case.k_pool, case.v_pool,
+                                       case.block_table, case.bt_stride, case.cu_seqlens_q, None, rows, 8, 8, 64, 2,
+                                       scale=0.2)
+    compare(case, out, lse, rows, ref, ref_lse, "scale0.2")
+    kp, vp = oracle.kv_append(case.k_new, case.v_new, case.k_pool, case.v_pool, case.block_table, case.bt_stride,
+                              case.cu_seqlens_q, None, 8, 64, 2)
+    np.testing.assert_array_equal(from_dev(case, dev.k_pool), kp)
+    np.testing.assert_array_equal(from_dev(case, dev.v_pool), vp)
+
+
+def test_no_op_and_error_paths_on_device():
+    case = dg.config("c1")
+    dev = Dev(case)
+    empty = torch.empty((0, 4, 64), dtype=torch.float32, device="cuda")
+    cu = torch.zeros(2, dtype=torch.int32, device="cuda")
+    out, _ = csr.extend_attention(dev.desc, empty, empty[:, :1], empty[:, :1], dev.k_pool, dev.v_pool, None,
+                                  case.bt_stride, cu, dev.cache_len, 0, 0, want_lse=False)
+    assert out.numel() == 0
+    with pytest.raises(csr.CsrError) as e:
+        csr.extend_attention(dev.desc, dev.q, dev.k_new, dev.v_new, dev.k_pool, dev.v_pool, None, case.bt_stride,
+                             dev.cu, dev.cache_len, case.max_seqlen_q + 1000, case.max_cache_len)
+    assert e.value.status == csr.CSR_E_INVAL
