@@ -41,9 +41,9 @@
  * enqueues nothing.  A launch error returns CSR_E_HIP.  csr_last_error() gives
  * a thread-local description of the last failure.  Block-table contents are a
  * caller contract: every page a call touches must be a valid id in
- * [0, num_pages); ids outside that range are neither read nor written (the key
- * is taken as zero, the append row is dropped) so a bad table cannot fault the
- * GPU, but the result is then unspecified.
+ * [0, num_pages); ids outside that range are never dereferenced (attention
+ * reads some other in-bounds key row in its place, the append row is dropped)
+ * so a bad table cannot fault the GPU, but the result is then unspecified.
  */
 #ifndef CSR_H
 #define CSR_H

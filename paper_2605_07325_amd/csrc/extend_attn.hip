@@ -274,13 +274,25 @@ __global__ void __launch_bounds__(512, 1) attn_bf16_kernel(const AttnArgs a) {
 
   // ---- DMA: lane's key row within the tile for block j, and its byte offset inside a token row.
   int drow[NDMA], dchunk[NDMA];
+  // Byte offsets of the lane's row inside a page (pool tiles) and inside the
+  // chunk's K/V rows (chunk tiles): with 64-key tiles aligned to 64, a page of
+  // P <= 64 keys starts the lane's in-page index at drow & (P-1); for P > 64
+  // the tile start inside the page is a scalar added separately.
+  int pool_off[NDMA], new_off[NDMA];
+  const int in_page_mask = min((1 << a.log2P) - 1, KT - 1);
 #pragma unroll
   for (int j = 0; j < NDMA; ++j) {
     drow[j] = (j * NW + wave) * ROWS_PER_KB + lane / NCH;
     dchunk[j] = u.g * ROWB + (chunk_of_slot<NCH>(drow[j], lane % NCH) << 4);
+    pool_off[j] = (drow[j] & in_page_mask) * (a.Hkv * ROWB) + dchunk[j];
+    new_off[j] = drow[j] * (a.Hkv * ROWB) + dchunk[j];
   }
-  // Page id of DMA block j of `tile` (wave-uniform in scalar mode; unused for chunk keys).
-  auto page_of = [&](int tile, int j) -> int {
+  // Byte offset, from the pool base, of the 64-key-aligned stretch of the page
+  // that holds DMA block j of `tile` (wave-uniform in scalar mode; per lane
+  // otherwise; unused for chunk keys).  Page ids outside [0, num_pages) read
+  // page 0 instead, so a bad table cannot send a load out of bounds.
+  const int64_t page_bytes = (int64_t)kv_stride << log2P;
+  auto page_of = [&](int tile, int j) -> int64_t {
     int t;
     if constexpr (SCALAR_PAGES)
       t = min(tile * KT + (j * NW + wave) * ROWS_PER_KB, last_key);
@@ -288,36 +300,37 @@ __global__ void __launch_bounds__(512, 1) attn_bf16_kernel(const AttnArgs a) {
       t = min(tile * KT + drow[j], last_key);
     if (t >= u.L) return 0;
     const int pidx = t >> log2P;
-    return bt ? bt[pidx] : bt_base + pidx;
+    int pg = bt ? bt[pidx] : bt_base + pidx;
+    pg = (pg >= 0 && pg < num_pages) ? pg : 0;
+    return (int64_t)(uint32_t)pg * page_bytes + (int64_t)((t & Pmask & ~(KT - 1)) * kv_stride);
   };
   auto dma = [&](const char* src, char* dst, int j) {
     __builtin_amdgcn_global_load_lds((const __attribute__((address_space(1))) void*)src,
                                      (__attribute__((address_space(3))) void*)(dst + (j * NW + wave) * 1024), 16, 0, 0);
   };
-  // DMA block j of a K or V tile into `dst`.  Pure-prefix and pure-chunk
-  // tiles take a scalar base plus a per-lane constant; a tile straddling L
-  // selects per lane.
-  auto issue_block = [&](int tile, int j, int pgj, char* dst, const char* pool_base, const char* new_base) {
+  // DMA block j of a K or V tile into `dst`.  A tile wholly inside the prefix
+  // or wholly inside the chunk takes a scalar base plus the lane's constant
+  // 32-bit offset; a tile straddling L or ending the key range selects per lane.
+  // (The empty asm markers keep the three loads apart: merged, their address
+  // would become a per-lane 64-bit value on every path.)
+  auto issue_block = [&](int tile, int j, int64_t pgoff, char* dst, const char* pool_base, const char* new_base) {
     const int t0 = tile * KT;
-    const int t_hi = min(t0 + KT - 1, last_key);
-    if (SCALAR_PAGES && t_hi < u.L) {
-      const bool ok = pgj >= 0 && pgj < num_pages;
-      const char* base = ok ? pool_base + (int64_t)pgj * ((int64_t)kv_stride << log2P)
-                            : new_base + (int64_t)u.cuq * kv_stride;  // bad page id: read a valid row instead
-      const int in_page = ok ? (((t0 & Pmask) + drow[j]) & Pmask) : 0;
-      dma(base + in_page * kv_stride + dchunk[j], dst, j);
-    } else if (t0 >= u.L) {
-      const char* base = new_base + (int64_t)(u.cuq + t0 - u.L) * kv_stride;
-      dma(base + min(drow[j], t_hi - t0) * kv_stride + dchunk[j], dst, j);
+    const uint32_t po = pool_off[j], no = new_off[j];
+    const int dr = drow[j], dc = dchunk[j];
+    if (t0 + KT - 1 < u.L) {
+      dma(pool_base + pgoff + po, dst, j);
+      asm volatile("; dma prefix tile");
+    } else if (t0 >= u.L && t0 + KT - 1 <= last_key) {
+      dma(new_base + (int64_t)(u.cuq + t0 - u.L) * kv_stride + no, dst, j);
+      asm volatile("; dma chunk tile");
     } else {
-      int t = min(t0 + drow[j], last_key);
-      const bool from_pool = t < u.L && pgj >= 0 && pgj < num_pages;
-      if (t < u.L && !from_pool) t = u.L;
-      const int64_t row = from_pool ? ((int64_t)pgj << log2P) + (t & Pmask) : (int64_t)(u.cuq + t - u.L);
-      dma((from_pool ? pool_base : new_base) + row * kv_stride + dchunk[j], dst, j);
+      const int t = min(t0 + dr, last_key);
+      const char* src = t < u.L ? pool_base + pgoff + po : new_base + (int64_t)(u.cuq + t - u.L) * kv_stride + dc;
+      dma(src, dst, j);
+      asm volatile("; dma mixed tile");
     }
   };
-  auto issue = [&](int tile, const int* pg, char* dst, const char* pool_base, const char* new_base) {
+  auto issue = [&](int tile, const int64_t* pg, char* dst, const char* pool_base, const char* new_base) {
 #pragma unroll
     for (int j = 0; j < NDMA; ++j) issue_block(tile, j, pg[j], dst, pool_base, new_base);
   };
@@ -416,29 +429,34 @@ __global__ void __launch_bounds__(512, 1) attn_bf16_kernel(const AttnArgs a) {
             __builtin_bit_cast(bf16x8, u32x4{w[hf][db][0][0], w[hf][db][0][1], w[hf][db][1][0], w[hf][db][1][1]}),
             __builtin_bit_cast(bf16x8, pf[hf]), o[db], 0, 0, 0);
   };
-  // exp2(s*c - m) packed to bf16 (two contraction halves of 8 keys); adds the row sums.
-  auto softmax_exp = [&](const f32x16& s, u32x4* pf) {
+  // exp2(s*c - m) packed to bf16 for contraction half hf (8 keys); adds the row sums.
+  auto exp_half = [&](const f32x16& s, int hf) -> u32x4 {
     const float neg_m = mref == -INFINITY ? 0.f : -mref;
+    float p[8];
     float rs = 0.f;
 #pragma unroll
-    for (int hf = 0; hf < 2; ++hf) {
-      float p[8];
-#pragma unroll
-      for (int e = 0; e < 8; ++e) {
-        p[e] = fast_exp2(__builtin_fmaf(s[8 * hf + e], c, neg_m));
-        rs += p[e];
-      }
-      pf[hf] = u32x4{pack_bf16x2(p[0], p[1]), pack_bf16x2(p[2], p[3]), pack_bf16x2(p[4], p[5]),
-                     pack_bf16x2(p[6], p[7])};
+    for (int e = 0; e < 8; ++e) {
+      p[e] = fast_exp2(__builtin_fmaf(s[8 * hf + e], c, neg_m));
+      rs += p[e];
     }
     lrow += rs;
+    return u32x4{pack_bf16x2(p[0], p[1]), pack_bf16x2(p[2], p[3]), pack_bf16x2(p[4], p[5]), pack_bf16x2(p[6], p[7])};
   };
+  auto softmax_exp = [&](const f32x16& s, u32x4* pf) {
+    pf[0] = exp_half(s, 0);
+    pf[1] = exp_half(s, 1);
+  };
+  // Pins a value at this point of the program: IR-level sinking would
+  // otherwise move the exponentials past the DMA branches to their use by the
+  // PV products, leaving them no score MFMAs to overlap with.
+  auto pin = [](u32x4& x) { asm volatile("" : "+v"(x)); };
   auto row_max = [&](const f32x16& s) -> float {
-    float mx = fmaxf(s[0], s[1]);
+    float mx = __builtin_elementwise_maximum(s[0], s[1]);
 #pragma unroll
-    for (int v = 2; v < 16; v += 2) mx = fmaxf(mx, fmaxf(s[v], s[v + 1]));
+    for (int v = 2; v < 16; v += 2)
+      mx = __builtin_elementwise_maximum(mx, __builtin_elementwise_maximum(s[v], s[v + 1]));
     const auto pr = __builtin_amdgcn_permlane32_swap(__float_as_uint(mx), __float_as_uint(mx), false, false);
-    return fmaxf(__uint_as_float(pr[0]), __uint_as_float(pr[1])) * c;
+    return __builtin_elementwise_maximum(__uint_as_float(pr[0]), __uint_as_float(pr[1])) * c;
   };
   // Move the reference max if any row of the wave grew past the threshold.
   auto update_ref = [&](float mxs) {
@@ -459,13 +477,16 @@ __global__ void __launch_bounds__(512, 1) attn_bf16_kernel(const AttnArgs a) {
   auto step = [&](f32x16& s_cur, f32x16& s_next, auto voff_c, const char* kl_next, int kb_next,
                   auto dma_a, auto dma_b) {
     u32x4 pf[2];
-    softmax_exp(s_cur, pf);
     s_next = f32x16{};
+    pf[0] = exp_half(s_cur, 0);
     qk_part(kl_next, kb_next, s_next, 0, DS / 2);
+    pin(pf[0]);
     __builtin_amdgcn_sched_barrier(0);
     dma_a();
     __builtin_amdgcn_sched_barrier(0);
+    pf[1] = exp_half(s_cur, 1);
     qk_part(kl_next, kb_next, s_next, DS / 2, DS);
+    pin(pf[1]);
     __builtin_amdgcn_sched_barrier(0);
     dma_b();
     __builtin_amdgcn_sched_barrier(0);
@@ -484,9 +505,9 @@ __global__ void __launch_bounds__(512, 1) attn_bf16_kernel(const AttnArgs a) {
     // last one and land in a stage nobody reads again), so "all but the
     // previous tile's loads" is the constant vmcnt(2*NDMA).
     auto clampt = [&](int t) { return min(t, main_end - 1); };
-    int pgn[NDMA];  // pages of tile tb+k+3, issued at tile k
+    int64_t pgn[NDMA];  // pages of tile tb+k+3, issued at tile k
     {
-      int pg[NDMA];
+      int64_t pg[NDMA];
 #pragma unroll
       for (int i = 0; i < 3; ++i) {
 #pragma unroll
@@ -545,7 +566,7 @@ __global__ void __launch_bounds__(512, 1) attn_bf16_kernel(const AttnArgs a) {
 
   // ---- tail: tiles [main_end, te) with the causal mask, one tile at a time
   for (int it = max(main_end, u.tb); it < u.te; ++it) {
-    int pg[NDMA];
+    int64_t pg[NDMA];
 #pragma unroll
     for (int j = 0; j < NDMA; ++j) pg[j] = page_of(it, j);
     issue(it, pg, kring, kpool, knew);
