@@ -56,9 +56,6 @@ typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
 typedef short s16x4 __attribute__((ext_vector_type(4)));
 typedef __attribute__((address_space(3))) s16x4 lds_s16x4;
 
-#ifndef CSR_SCHED
-#define CSR_SCHED 2  // instruction interleaving of the pipelined main loop (0: compiler default)
-#endif
 
 constexpr int KT = 64;        // keys per tile
 constexpr int NTHREADS = 256;  // 4 waves
@@ -292,18 +289,26 @@ __global__ void __launch_bounds__(512, 1) attn_bf16_kernel(const AttnArgs a) {
   // otherwise; unused for chunk keys).  Page ids outside [0, num_pages) read
   // page 0 instead, so a bad table cannot send a load out of bounds.
   const int64_t page_bytes = (int64_t)kv_stride << log2P;
-  auto page_of = [&](int tile, int j) -> int64_t {
-    int t;
+  auto block_key = [&](int tile, int j) -> int {
     if constexpr (SCALAR_PAGES)
-      t = min(tile * KT + (j * NW + wave) * ROWS_PER_KB, last_key);
+      return min(tile * KT + (j * NW + wave) * ROWS_PER_KB, last_key);
     else
-      t = min(tile * KT + drow[j], last_key);
+      return min(tile * KT + drow[j], last_key);
+  };
+  // Split in two so that the block-table load can be issued well before the
+  // offset is needed: page_id loads, page_off does the arithmetic.
+  auto page_id = [&](int tile, int j) -> int {
+    const int t = block_key(tile, j);
     if (t >= u.L) return 0;
     const int pidx = t >> log2P;
-    int pg = bt ? bt[pidx] : bt_base + pidx;
+    return bt ? bt[pidx] : bt_base + pidx;
+  };
+  auto page_off = [&](int tile, int j, int pg) -> int64_t {
+    const int t = block_key(tile, j);
     pg = (pg >= 0 && pg < num_pages) ? pg : 0;
     return (int64_t)(uint32_t)pg * page_bytes + (int64_t)((t & Pmask & ~(KT - 1)) * kv_stride);
   };
+  auto page_of = [&](int tile, int j) -> int64_t { return page_off(tile, j, page_id(tile, j)); };
   auto dma = [&](const char* src, char* dst, int j) {
     __builtin_amdgcn_global_load_lds((const __attribute__((address_space(1))) void*)src,
                                      (__attribute__((address_space(3))) void*)(dst + (j * NW + wave) * 1024), 16, 0, 0);
@@ -318,10 +323,16 @@ __global__ void __launch_bounds__(512, 1) attn_bf16_kernel(const AttnArgs a) {
     const uint32_t po = pool_off[j], no = new_off[j];
     const int dr = drow[j], dc = dchunk[j];
     if (t0 + KT - 1 < u.L) {
-      dma(pool_base + pgoff + po, dst, j);
+      // The opaque scalar base keeps the sum in SGPRs: otherwise the
+      // loop-invariant pool_base + po is hoisted into a 64-bit VGPR pair.
+      const char* base = pool_base + pgoff;
+      if constexpr (SCALAR_PAGES) asm("" : "+s"(base));
+      dma(base + po, dst, j);
       asm volatile("; dma prefix tile");
     } else if (t0 >= u.L && t0 + KT - 1 <= last_key) {
-      dma(new_base + (int64_t)(u.cuq + t0 - u.L) * kv_stride + no, dst, j);
+      const char* base = new_base + (int64_t)(u.cuq + t0 - u.L) * kv_stride;
+      asm("" : "+s"(base));
+      dma(base + no, dst, j);
       asm volatile("; dma chunk tile");
     } else {
       const int t = min(t0 + dr, last_key);
@@ -334,9 +345,11 @@ __global__ void __launch_bounds__(512, 1) attn_bf16_kernel(const AttnArgs a) {
 #pragma unroll
     for (int j = 0; j < NDMA; ++j) issue_block(tile, j, pg[j], dst, pool_base, new_base);
   };
-  char* const vring = lds;
-  char* const kring = lds + ST * TILEB;
-  const uint32_t lds_addr = (uint32_t)(size_t)((__attribute__((address_space(3))) char*)lds);
+  // K ring first: its stage and block offsets then fit the 16-bit DS offset
+  // field; the V ring's base is folded into the per-lane V read addresses.
+  char* const kring = lds;
+  char* const vring = lds + ST * TILEB;
+  const uint32_t vring_addr = (uint32_t)(size_t)((__attribute__((address_space(3))) char*)vring);
 
   // Per-lane LDS read offsets (stage and 32-key block offsets are added as immediates).
   int koff[DS];
@@ -359,15 +372,21 @@ __global__ void __launch_bounds__(512, 1) attn_bf16_kernel(const AttnArgs a) {
 #pragma unroll
   for (int db = 0; db < DB; ++db) o[db] = f32x16{};
   float mref = -INFINITY, lrow = 0.f;
+  // -mref (0 while no key has been seen), and the per-lane score above which
+  // the reference must move: (mref + THRESH) / c.
+  float neg_m = 0.f, thr = -INFINITY;
 
   // Scores of 32-key block kb of a K tile: S^T[key][row] (contraction steps [d0, d1)).
-  auto qk_part = [&](const char* kl, int kb, f32x16& s, int d0, int d1) {
+  // K fragments of k-steps [d0, d0 + DS/2) of block kb, and the score MFMAs over them.
+  auto load_k = [&](const char* kl, int kb, int d0, u32x4* kf) {
 #pragma unroll
-    for (int ds = d0; ds < d1; ++ds) {
-      const u32x4 kf = *reinterpret_cast<const u32x4*>(kl + kb * 32 * ROWB + koff[ds]);
-      s = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, kf), __builtin_bit_cast(bf16x8, qf[ds]),
+    for (int i = 0; i < DS / 2; ++i) kf[i] = *reinterpret_cast<const u32x4*>(kl + kb * 32 * ROWB + koff[d0 + i]);
+  };
+  auto mfma_k = [&](const u32x4* kf, int d0, f32x16& s) {
+#pragma unroll
+    for (int i = 0; i < DS / 2; ++i)
+      s = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, kf[i]), __builtin_bit_cast(bf16x8, qf[d0 + i]),
                                                   s, 0, 0, 0);
-    }
   };
   auto qk = [&](const char* kl, int kb, f32x16& s) {
     s = f32x16{};
@@ -407,8 +426,8 @@ __global__ void __launch_bounds__(512, 1) attn_bf16_kernel(const AttnArgs a) {
     for (int hf = 0; hf < 2; ++hf)
 #pragma unroll
       for (int db = 0; db < DB; ++db) {
-        asm volatile("ds_read_b64_tr_b16 %0, %1 offset:%2" : "=v"(w[hf][db][0]) : "v"(lds_addr + voff_a[db]), "i"(VOFF + hf * 16 * ROWB));
-        asm volatile("ds_read_b64_tr_b16 %0, %1 offset:%2" : "=v"(w[hf][db][1]) : "v"(lds_addr + voff_b[db]), "i"(VOFF + hf * 16 * ROWB));
+        asm volatile("ds_read_b64_tr_b16 %0, %1 offset:%2" : "=v"(w[hf][db][0]) : "v"(vring_addr + voff_a[db]), "i"(VOFF + hf * 16 * ROWB));
+        asm volatile("ds_read_b64_tr_b16 %0, %1 offset:%2" : "=v"(w[hf][db][1]) : "v"(vring_addr + voff_b[db]), "i"(VOFF + hf * 16 * ROWB));
       }
     if constexpr (DB == 4) {
       asm volatile("s_waitcnt lgkmcnt(0)"
@@ -431,16 +450,15 @@ __global__ void __launch_bounds__(512, 1) attn_bf16_kernel(const AttnArgs a) {
   };
   // exp2(s*c - m) packed to bf16 for contraction half hf (8 keys); adds the row sums.
   auto exp_half = [&](const f32x16& s, int hf) -> u32x4 {
-    const float neg_m = mref == -INFINITY ? 0.f : -mref;
     float p[8];
+#pragma unroll
+    for (int e = 0; e < 8; ++e) p[e] = fast_exp2(__builtin_fmaf(s[8 * hf + e], c, neg_m));
+    const u32x4 r{pack_bf16x2(p[0], p[1]), pack_bf16x2(p[2], p[3]), pack_bf16x2(p[4], p[5]), pack_bf16x2(p[6], p[7])};
     float rs = 0.f;
 #pragma unroll
-    for (int e = 0; e < 8; ++e) {
-      p[e] = fast_exp2(__builtin_fmaf(s[8 * hf + e], c, neg_m));
-      rs += p[e];
-    }
+    for (int e = 0; e < 8; ++e) rs += p[e];
     lrow += rs;
-    return u32x4{pack_bf16x2(p[0], p[1]), pack_bf16x2(p[2], p[3]), pack_bf16x2(p[4], p[5]), pack_bf16x2(p[6], p[7])};
+    return r;
   };
   auto softmax_exp = [&](const f32x16& s, u32x4* pf) {
     pf[0] = exp_half(s, 0);
@@ -450,23 +468,28 @@ __global__ void __launch_bounds__(512, 1) attn_bf16_kernel(const AttnArgs a) {
   // otherwise move the exponentials past the DMA branches to their use by the
   // PV products, leaving them no score MFMAs to overlap with.
   auto pin = [](u32x4& x) { asm volatile("" : "+v"(x)); };
+  // Maximum of the lane's 16 raw scores (half of its row's 32 keys).
   auto row_max = [&](const f32x16& s) -> float {
     float mx = __builtin_elementwise_maximum(s[0], s[1]);
 #pragma unroll
     for (int v = 2; v < 16; v += 2)
       mx = __builtin_elementwise_maximum(mx, __builtin_elementwise_maximum(s[v], s[v + 1]));
-    const auto pr = __builtin_amdgcn_permlane32_swap(__float_as_uint(mx), __float_as_uint(mx), false, false);
-    return __builtin_elementwise_maximum(__uint_as_float(pr[0]), __uint_as_float(pr[1])) * c;
+    return mx;
   };
-  // Move the reference max if any row of the wave grew past the threshold.
-  auto update_ref = [&](float mxs) {
-    if (__any(mxs > mref + THRESH)) {
+  // Move the reference max if any lane's scores grew past the threshold; only
+  // then is the exact row max (both half-rows) formed.
+  auto update_ref = [&](float mx) {
+    if (__any(mx > thr)) {
+      const auto pr = __builtin_amdgcn_permlane32_swap(__float_as_uint(mx), __float_as_uint(mx), false, false);
+      const float mxs = __builtin_elementwise_maximum(__uint_as_float(pr[0]), __uint_as_float(pr[1])) * c;
       const float mnew = fmaxf(mref, mxs);
       const float alpha = fast_exp2((mref == -INFINITY ? 0.f : mref) - (mnew == -INFINITY ? 0.f : mnew));
       lrow *= alpha;
 #pragma unroll
       for (int db = 0; db < DB; ++db) o[db] *= alpha;
       mref = mnew;
+      neg_m = mnew == -INFINITY ? 0.f : -mnew;
+      thr = (mnew + THRESH) / c;
     }
   };
   // One pipelined block step: exponentials of s_cur (block kb of V tile vl)
@@ -474,21 +497,29 @@ __global__ void __launch_bounds__(512, 1) attn_bf16_kernel(const AttnArgs a) {
   // Each step also issues two DMA blocks (dma_a, dma_b), one after each half
   // of the score MFMAs, so each wave's loads trickle into the memory pipeline
   // instead of arriving with every other wave's at the tile boundary.
+  // K fragments of the first half of the next step's score block, read one
+  // group of products ahead so that their LDS latency hides behind MFMAs.
+  u32x4 kpre[DS / 2];
   auto step = [&](f32x16& s_cur, f32x16& s_next, auto voff_c, const char* kl_next, int kb_next,
-                  auto dma_a, auto dma_b) {
+                  const char* kl_after, int kb_after, auto dma_a, auto dma_b) {
     u32x4 pf[2];
+    u32x4 kh1[DS / 2];
     s_next = f32x16{};
+    load_k(kl_next, kb_next, DS / 2, kh1);
+    __builtin_amdgcn_sched_barrier(0);
     pf[0] = exp_half(s_cur, 0);
-    qk_part(kl_next, kb_next, s_next, 0, DS / 2);
+    mfma_k(kpre, 0, s_next);
     pin(pf[0]);
     __builtin_amdgcn_sched_barrier(0);
     dma_a();
     __builtin_amdgcn_sched_barrier(0);
     pf[1] = exp_half(s_cur, 1);
-    qk_part(kl_next, kb_next, s_next, DS / 2, DS);
+    mfma_k(kh1, DS / 2, s_next);
     pin(pf[1]);
     __builtin_amdgcn_sched_barrier(0);
     dma_b();
+    __builtin_amdgcn_sched_barrier(0);
+    load_k(kl_after, kb_after, 0, kpre);
     __builtin_amdgcn_sched_barrier(0);
     pv_asm(voff_c, pf);
     update_ref(row_max(s_next));
@@ -505,7 +536,8 @@ __global__ void __launch_bounds__(512, 1) attn_bf16_kernel(const AttnArgs a) {
     // last one and land in a stage nobody reads again), so "all but the
     // previous tile's loads" is the constant vmcnt(2*NDMA).
     auto clampt = [&](int t) { return min(t, main_end - 1); };
-    int64_t pgn[NDMA];  // pages of tile tb+k+3, issued at tile k
+    int64_t pgn[NDMA];  // page offsets of tile tb+k+3, issued at tile k
+    int pgi[NDMA];      // their raw page ids, loaded half a tile earlier
     {
       int64_t pg[NDMA];
 #pragma unroll
@@ -516,13 +548,14 @@ __global__ void __launch_bounds__(512, 1) attn_bf16_kernel(const AttnArgs a) {
         issue(clampt(u.tb + i), pg, vring + i * TILEB, vpool, vnew);
       }
 #pragma unroll
-      for (int j = 0; j < NDMA; ++j) pgn[j] = page_of(clampt(u.tb + 3), j);
+      for (int j = 0; j < NDMA; ++j) pgi[j] = page_id(clampt(u.tb + 3), j);
     }
     asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
     __syncthreads();
     f32x16 s_a, s_b;
     qk(kring, 0, s_a);
     update_ref(row_max(s_a));
+    load_k(kring, 1, 0, kpre);
     // Tile k with ring stage S = k % 4 known at compile time.
     auto tile = [&](int k, auto stage) {
       constexpr int S = decltype(stage)::value;
@@ -536,6 +569,8 @@ __global__ void __launch_bounds__(512, 1) attn_bf16_kernel(const AttnArgs a) {
       // K/V(tb+k+3) replace K/V(tb+k-1), last read during tile k-1; their
       // DMA blocks are spread over the tile's two steps.
       const int nt = clampt(u.tb + k + 3);
+#pragma unroll
+      for (int j = 0; j < NDMA; ++j) pgn[j] = page_off(nt, j, pgi[j]);
       char* kdst = kring + ((S + 3) % ST) * TILEB;
       char* vdst = vring + ((S + 3) % ST) * TILEB;
       const char* kl = kring + S * TILEB;
@@ -545,11 +580,16 @@ __global__ void __launch_bounds__(512, 1) attn_bf16_kernel(const AttnArgs a) {
       auto vd1 = [&] {
         if constexpr (NDMA > 1) issue_block(nt, NDMA - 1, pgn[NDMA - 1], vdst, vpool, vnew);
 #pragma unroll
-        for (int j = 0; j < NDMA; ++j) pgn[j] = page_of(clampt(u.tb + k + 4), j);
+        for (int j = 0; j < NDMA; ++j) pgi[j] = page_id(clampt(u.tb + k + 4), j);
       };
+      // The two waves of a SIMD take turns at the higher issue priority, one
+      // step each, so that neither lags the other into the tile barrier.
+      if (wave < NW / 2) __builtin_amdgcn_s_setprio(1); else __builtin_amdgcn_s_setprio(0);
       // block 0 || scores of block 1, then block 1 || scores of the next tile's block 0
-      step(s_a, s_b, std::integral_constant<int, S * TILEB>{}, kl, 1, kd0, kd1);
-      step(s_a, s_b, std::integral_constant<int, S * TILEB + 32 * ROWB>{}, kring + ((S + 1) % ST) * TILEB, 0, vd0, vd1);
+      step(s_a, s_b, std::integral_constant<int, S * TILEB>{}, kl, 1, kring + ((S + 1) % ST) * TILEB, 0, kd0, kd1);
+      if (wave < NW / 2) __builtin_amdgcn_s_setprio(0); else __builtin_amdgcn_s_setprio(1);
+      step(s_a, s_b, std::integral_constant<int, S * TILEB + 32 * ROWB>{}, kring + ((S + 1) % ST) * TILEB, 0,
+           kring + ((S + 1) % ST) * TILEB, 1, vd0, vd1);
     };
     for (int k = 0; k < n_main; k += 4) {
       tile(k, std::integral_constant<int, 0>{});
@@ -560,6 +600,7 @@ __global__ void __launch_bounds__(512, 1) attn_bf16_kernel(const AttnArgs a) {
       if (k + 3 >= n_main) break;
       tile(k + 3, std::integral_constant<int, 3>{});
     }
+    __builtin_amdgcn_s_setprio(0);
     asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
     __syncthreads();  // every wave is done with the rings before the tail reuses them
   }
