@@ -258,6 +258,10 @@ __global__ void __launch_bounds__(512, 1) attn_bf16_kernel(const AttnArgs a) {
   u32x4 qf[DS];
   const int m_row = u.m0 + wave * 32 + l32;
   const bool valid = m_row < u.rows_total;
+  // A wave whose 32 rows are all padding (short chunks: n*G < BM) skips the
+  // products and exponentials but still issues its share of every K/V DMA
+  // and joins every barrier.
+  const bool wave_active = u.m0 + wave * 32 < u.rows_total;
   const int tok = m_row / G;
   const int lim = u.L + tok;  // last key this lane's row sees
   {
@@ -553,9 +557,11 @@ __global__ void __launch_bounds__(512, 1) attn_bf16_kernel(const AttnArgs a) {
     asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
     __syncthreads();
     f32x16 s_a, s_b;
-    qk(kring, 0, s_a);
-    update_ref(row_max(s_a));
-    load_k(kring, 1, 0, kpre);
+    if (wave_active) {
+      qk(kring, 0, s_a);
+      update_ref(row_max(s_a));
+      load_k(kring, 1, 0, kpre);
+    }
     // Tile k with ring stage S = k % 4 known at compile time.
     auto tile = [&](int k, auto stage) {
       constexpr int S = decltype(stage)::value;
@@ -586,6 +592,10 @@ __global__ void __launch_bounds__(512, 1) attn_bf16_kernel(const AttnArgs a) {
       // step each, so that neither lags the other into the tile barrier.
       if (wave < NW / 2) __builtin_amdgcn_s_setprio(1); else __builtin_amdgcn_s_setprio(0);
       // block 0 || scores of block 1, then block 1 || scores of the next tile's block 0
+      if (!wave_active) {
+        kd0(); kd1(); vd0(); vd1();
+        return;
+      }
       step(s_a, s_b, std::integral_constant<int, S * TILEB>{}, kl, 1, kring + ((S + 1) % ST) * TILEB, 0, kd0, kd1);
       if (wave < NW / 2) __builtin_amdgcn_s_setprio(0); else __builtin_amdgcn_s_setprio(1);
       step(s_a, s_b, std::integral_constant<int, S * TILEB + 32 * ROWB>{}, kring + ((S + 1) % ST) * TILEB, 0,
@@ -616,7 +626,7 @@ __global__ void __launch_bounds__(512, 1) attn_bf16_kernel(const AttnArgs a) {
     __syncthreads();
     const int t0 = it * KT;
 #pragma unroll
-    for (int kb = 0; kb < 2; ++kb) {
+    for (int kb = 0; kb < 2 && wave_active; ++kb) {
       f32x16 s;
       qk(kring, kb, s);
       if (t0 + kb * 32 + 31 > lim) {

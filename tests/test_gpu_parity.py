@@ -20,11 +20,12 @@ pytestmark = pytest.mark.gpu
 
 @pytest.fixture(autouse=True)
 def _no_split_override():
-    saved = os.environ.pop("CSR_NSPLIT", None)
+    saved = {k: os.environ.pop(k, None) for k in ("CSR_NSPLIT",)}
     yield
-    os.environ.pop("CSR_NSPLIT", None)
-    if saved is not None:
-        os.environ["CSR_NSPLIT"] = saved
+    for k, v in saved.items():
+        os.environ.pop(k, None)
+        if v is not None:
+            os.environ[k] = v
 
 
 SMALL = [
@@ -134,3 +135,47 @@ def test_c5_ragged_batch_with_append():
                               case.cu_seqlens_q, case.cache_len, case.num_kv_heads, case.head_dim, case.page_size)
     np.testing.assert_array_equal(from_dev(case, dev.k_pool), kp)
     np.testing.assert_array_equal(from_dev(case, dev.v_pool), vp)
+
+
+# Short chunks (decode-like: at most 128 packed rows per unit), where most
+# waves of a workgroup hold only padding rows and skip the products.
+DECODE = [
+    ("decode_ragged_append", dict(dtype=dg.BF16, num_q_heads=64, num_kv_heads=4, head_dim=128,
+                                  cache_len=[4096, 17, 1000, 333], seqlen_q=[1, 8, 3, 5], page_size=16, scale=0.5,
+                                  interleave=True)),
+    ("decode_d64_pages4", dict(dtype=dg.BF16, num_q_heads=32, num_kv_heads=4, head_dim=64, cache_len=[2000, 64],
+                               seqlen_q=[2, 16], page_size=4, scale=0.5)),
+    ("decode_g2_rows40", dict(dtype=dg.BF16, num_q_heads=8, num_kv_heads=4, head_dim=128, cache_len=[700, 0, 95],
+                              seqlen_q=[20, 7, 1], page_size=8, scale=0.5)),
+]
+
+
+@pytest.mark.parametrize("label,kw", DECODE, ids=[d[0] for d in DECODE])
+@pytest.mark.parametrize("nsplit", [None, 5])
+def test_short_chunks_all_rows(label, kw, nsplit):
+    if nsplit:
+        os.environ["CSR_NSPLIT"] = str(nsplit)
+    case = dg.make_case(label, seed=2, cfg_id=310, **kw)
+    note(f"{label} nsplit={nsplit} L={case.cache_len.tolist()} n={case.seqlen_q.tolist()}")
+    dev = Dev(case)
+    out, lse = dev.extend(append=True)
+    torch.cuda.synchronize()
+    rows = np.arange(case.total_q, dtype=np.int32)
+    ref, ref_lse = oracle_rows(case, rows)
+    compare(case, out, lse, rows, ref, ref_lse, f"{label}/split={nsplit}")
+    kp, vp = oracle.kv_append(case.k_new, case.v_new, case.k_pool, case.v_pool, case.block_table, case.bt_stride,
+                              case.cu_seqlens_q, case.cache_len, case.num_kv_heads, case.head_dim, case.page_size)
+    np.testing.assert_array_equal(from_dev(case, dev.k_pool), kp)
+    np.testing.assert_array_equal(from_dev(case, dev.v_pool), vp)
+
+
+@pytest.mark.parametrize("n", [1, 8])
+def test_c3_decode_120k_prefix_all_rows(n):
+    case = dg.config(f"c3_{n}")
+    note(f"c3 bf16 L=122880 n={n} (decode-like chunk): csr_extend_attention")
+    dev = Dev(case)
+    out, lse = dev.extend()
+    torch.cuda.synchronize()
+    rows = np.arange(case.total_q, dtype=np.int32)
+    ref, ref_lse = oracle_rows(case, rows)
+    compare(case, out, lse, rows, ref, ref_lse, f"c3_{n}")
