@@ -151,7 +151,7 @@ DECODE = [
 
 
 @pytest.mark.parametrize("label,kw", DECODE, ids=[d[0] for d in DECODE])
-@pytest.mark.parametrize("nsplit", [None, 5])
+@pytest.mark.parametrize("nsplit", [None, 5, 16])
 def test_short_chunks_all_rows(label, kw, nsplit):
     if nsplit:
         os.environ["CSR_NSPLIT"] = str(nsplit)
