@@ -26,6 +26,16 @@
  * rescaling.  bf16 inputs are widened exactly (a bf16 value is the upper 16
  * bits of an IEEE binary32 value).
  *
+ * Rotary position embedding (optional; not part of the paper's equations,
+ * which take k_n and q_n as the projections of eq. (k) and its query
+ * counterpart): RoFormer's rotation (Su et al., 2021) applied to q_n and k_n at
+ * their absolute cache position n before they enter the attention and the
+ * cache.  The first r dims form r/2 pairs; pair i turns by the angle
+ * pos * base^(-2i/r).  Two pairings are in use: "neox" pairs dim i with
+ * dim i + r/2, "interleaved" pairs dim 2i with dim 2i + 1.  Dims >= r pass
+ * through.  Keys already in the cache were rotated when they were appended, so
+ * they are used as stored.
+ *
  * Paged cache layout (the library's contract; one convention for both sides):
  *   pool[num_pages][P][Hkv][d]; logical position t of sequence b lives in
  *   slot = page * P + (t mod P), page = block_table[b * bt_stride + t / P];
@@ -41,6 +51,59 @@
 #endif
 
 enum { ORACLE_F32 = 0, ORACLE_BF16 = 1 };
+enum { ROPE_NONE = 0, ROPE_NEOX = 1, ROPE_INTERLEAVED = 2 };
+
+/*
+ * Rotate one d-vector for absolute position pos (RoFormer's rotary position
+ * embedding, see the file comment).  Plain double-precision evaluation of the
+ * definition: angle = pos * base^(-2i/r), libm cos/sin.  y may not alias x.
+ */
+static void rope_row(const double* x, double* y, int d, int r, int style, double base, int64_t pos) {
+  for (int c = 0; c < d; ++c) y[c] = x[c];
+  if (style == ROPE_NONE) return;
+  for (int i = 0; i < r / 2; ++i) {
+    const double angle = (double)pos * pow(base, -2.0 * i / r);
+    const double cs = cos(angle), sn = sin(angle);
+    const int a = style == ROPE_NEOX ? i : 2 * i;
+    const int b = style == ROPE_NEOX ? i + r / 2 : 2 * i + 1;
+    y[a] = x[a] * cs - x[b] * sn;
+    y[b] = x[b] * cs + x[a] * sn;
+  }
+}
+
+/* Round a double to the nearest bf16 value (ties to even), returned as its
+ * 16-bit pattern.  Direct from double: no intermediate rounding to float. */
+static uint16_t bf16_from_double(double v) {
+  if (isnan(v)) return 0x7fc0;
+  const int neg = signbit(v) != 0;
+  double a = fabs(v);
+  double q;
+  if (a == 0.0 || isinf(a)) {
+    q = a;
+  } else {
+    int e;
+    (void)frexp(a, &e);               /* a = m * 2^e, m in [0.5, 1) */
+    int step = e - 8;                 /* 8 significant bits: spacing 2^(e-8) */
+    if (step < -133) step = -133;     /* subnormal spacing */
+    q = ldexp(nearbyint(ldexp(a, -step)), step);  /* default rounding: ties to even */
+    if (q > 3.3895313892515355e38) q = INFINITY;  /* above the largest bf16 */
+  }
+  const float f = (float)(neg ? -q : q);  /* exact: q is a bf16 value */
+  uint32_t bits;
+  memcpy(&bits, &f, sizeof bits);
+  return (uint16_t)(bits >> 16);
+}
+
+/*
+ * Rotate n_rows d-vectors, row k at position pos[k] (fp64 in, fp64 out).
+ * Returns -1 for a malformed rotation (odd or out-of-range r, unknown pairing).
+ */
+int csr_oracle_rope(const double* x, double* y, int64_t n_rows, int d, int r, int style, double base,
+                    const int64_t* pos) {
+  if (style < ROPE_NONE || style > ROPE_INTERLEAVED || r < 2 || r > d || (r & 1)) return -1;
+  for (int64_t k = 0; k < n_rows; ++k) rope_row(x + k * d, y + k * d, d, r, style, base, pos[k]);
+  return 0;
+}
 
 static double widen(const void* base, int64_t idx, int dtype) {
   if (dtype == ORACLE_BF16) {
@@ -69,10 +132,13 @@ static int owner(const int32_t* cu, int batch, int tok) {
  * Attention for the query tokens listed in `rows` (indices into the packed
  * [T_q, Hq, d] query array), all heads.  out: [n_rows, Hq, d], lse: [n_rows, Hq],
  * pairs: [n_rows, Hq] number of (query, key) pairs evaluated.  cache_len may be
- * NULL (every L_b = 0: prefill).  Returns 0, or -1 for a token outside every
- * sequence, or -2 on allocation failure.
+ * NULL (every L_b = 0: prefill).  rope_style != ROPE_NONE rotates each query
+ * row and each chunk key (t >= L_b) at its absolute position (rope_dim dims,
+ * base rope_theta); cached keys are used as stored.  Returns 0, or -1 for a
+ * token outside every sequence, or -2 on allocation failure.
  */
-int csr_oracle_attention(int dtype, int Hq, int Hkv, int d, int P, double scale, int batch,
+int csr_oracle_attention(int dtype, int Hq, int Hkv, int d, int P, double scale, int rope_style,
+                         int rope_dim, double rope_theta, int batch,
                          const void* q, const void* k_new, const void* v_new, const void* k_pool,
                          const void* v_pool, const int32_t* block_table, int bt_stride,
                          const int32_t* cu_seqlens_q, const int32_t* cache_len, int n_rows,
@@ -98,25 +164,29 @@ int csr_oracle_attention(int dtype, int Hq, int Hkv, int d, int P, double scale,
     double* s = (double*)malloc(sizeof(double) * (size_t)(G * nkeys));
     double* qv = (double*)malloc(sizeof(double) * (size_t)(G * d));
     double* kv = (double*)malloc(sizeof(double) * (size_t)d);
+    double* raw = (double*)malloc(sizeof(double) * (size_t)d);
     double* acc = (double*)calloc((size_t)(G * d), sizeof(double));
-    if (!s || !qv || !kv || !acc) {
-      free(s); free(qv); free(kv); free(acc);
+    if (!s || !qv || !kv || !raw || !acc) {
+      free(s); free(qv); free(kv); free(raw); free(acc);
 #ifdef _OPENMP
 #pragma omp atomic write
 #endif
       status = -2;
       continue;
     }
-    for (int j = 0; j < G; ++j)
-      for (int c = 0; c < d; ++c)
-        qv[j * d + c] = widen(q, ((int64_t)tok * Hq + g * G + j) * d + c, dtype);
+    for (int j = 0; j < G; ++j) {
+      for (int c = 0; c < d; ++c) raw[c] = widen(q, ((int64_t)tok * Hq + g * G + j) * d + c, dtype);
+      rope_row(raw, qv + j * d, d, rope_dim, rope_style, rope_theta, L + i);
+    }
     /* pass 1: scores */
     for (int64_t t = 0; t < nkeys; ++t) {
       int64_t base;
       const void* ksrc;
       if (t < L) { base = (cache_slot(block_table, bt_stride, P, b, t) * Hkv + g) * d; ksrc = k_pool; }
       else       { base = ((int64_t)(cu_seqlens_q[b] + (t - L)) * Hkv + g) * d; ksrc = k_new; }
-      for (int c = 0; c < d; ++c) kv[c] = widen(ksrc, base + c, dtype);
+      for (int c = 0; c < d; ++c) raw[c] = widen(ksrc, base + c, dtype);
+      if (t < L) memcpy(kv, raw, sizeof(double) * (size_t)d);
+      else rope_row(raw, kv, d, rope_dim, rope_style, rope_theta, t);
       for (int j = 0; j < G; ++j) {
         double dot = 0.0;
         for (int c = 0; c < d; ++c) dot += qv[j * d + c] * kv[c];
@@ -151,29 +221,49 @@ int csr_oracle_attention(int dtype, int Hq, int Hkv, int d, int P, double scale,
       lse[(int64_t)r * Hq + h] = m[j] + log(l[j]);
       pairs[(int64_t)r * Hq + h] = nkeys;
     }
-    free(s); free(qv); free(kv); free(acc);
+    free(s); free(qv); free(kv); free(raw); free(acc);
   }
   return status;
 }
 
 /*
  * Append oracle (the paper's append-only growth T_{t+1} = T_t (+) dX_t,
- * Theorem 2): chunk row i of sequence b is copied bit for bit into cache
- * position L_b + i; no other byte of either pool changes.
+ * Theorem 2): chunk row i of sequence b goes to cache position L_b + i; no
+ * other byte of either pool changes.  Values are copied bit for bit; keys too
+ * unless rope_style != ROPE_NONE, in which case each key row is first rotated
+ * at its position L_b + i (in double precision) and rounded to the pool's
+ * element type (nearest, ties to even).
  */
-int csr_oracle_kv_append(int elem_bytes, int Hkv, int d, int P, int batch, const void* k_new,
-                         const void* v_new, void* k_pool, void* v_pool,
-                         const int32_t* block_table, int bt_stride, const int32_t* cu_seqlens_q,
-                         const int32_t* cache_len) {
+int csr_oracle_kv_append(int dtype, int Hkv, int d, int P, int rope_style, int rope_dim,
+                         double rope_theta, int batch, const void* k_new, const void* v_new,
+                         void* k_pool, void* v_pool, const int32_t* block_table, int bt_stride,
+                         const int32_t* cu_seqlens_q, const int32_t* cache_len) {
+  const int elem_bytes = dtype == ORACLE_BF16 ? 2 : 4;
   const size_t row = (size_t)Hkv * d * elem_bytes; /* one token: all kv heads */
+  double* raw = (double*)malloc(sizeof(double) * (size_t)d);
+  double* rot = (double*)malloc(sizeof(double) * (size_t)d);
+  if (!raw || !rot) { free(raw); free(rot); return -2; }
   for (int b = 0; b < batch; ++b) {
     const int64_t L = cache_len ? cache_len[b] : 0;
     for (int64_t i = 0; i < cu_seqlens_q[b + 1] - cu_seqlens_q[b]; ++i) {
       const int64_t slot = cache_slot(block_table, bt_stride, P, b, L + i);
       const int64_t src = cu_seqlens_q[b] + i;
-      memcpy((char*)k_pool + slot * row, (const char*)k_new + src * row, row);
       memcpy((char*)v_pool + slot * row, (const char*)v_new + src * row, row);
+      if (rope_style == ROPE_NONE) {
+        memcpy((char*)k_pool + slot * row, (const char*)k_new + src * row, row);
+        continue;
+      }
+      for (int g = 0; g < Hkv; ++g) {
+        for (int c = 0; c < d; ++c) raw[c] = widen(k_new, (src * Hkv + g) * d + c, dtype);
+        rope_row(raw, rot, d, rope_dim, rope_style, rope_theta, L + i);
+        for (int c = 0; c < d; ++c) {
+          const int64_t e = (slot * Hkv + g) * d + c;
+          if (dtype == ORACLE_BF16) ((uint16_t*)k_pool)[e] = bf16_from_double(rot[c]);
+          else ((float*)k_pool)[e] = (float)rot[c];
+        }
+      }
     }
   }
+  free(raw); free(rot);
   return 0;
 }

@@ -16,6 +16,7 @@ SRC = os.path.join(HERE, "csr_oracle.c")
 LIB = os.path.join(HERE, "liboracle.so")
 
 F32, BF16 = 0, 1
+ROPE_NONE, ROPE_NEOX, ROPE_INTERLEAVED = 0, 1, 2
 
 _lib = None
 
@@ -35,10 +36,13 @@ def _load():
             build()
         lib = ctypes.CDLL(LIB)
         p, i, d = ctypes.c_void_p, ctypes.c_int, ctypes.c_double
-        lib.csr_oracle_attention.argtypes = [i, i, i, i, i, d, i, p, p, p, p, p, p, i, p, p, i, p, p, p, p, i]
+        lib.csr_oracle_attention.argtypes = [i, i, i, i, i, d, i, i, d, i, p, p, p, p, p, p, i, p, p, i, p, p, p,
+                                             p, i]
         lib.csr_oracle_attention.restype = i
-        lib.csr_oracle_kv_append.argtypes = [i, i, i, i, i, p, p, p, p, p, i, p, p]
+        lib.csr_oracle_kv_append.argtypes = [i, i, i, i, i, i, d, i, p, p, p, p, p, i, p, p]
         lib.csr_oracle_kv_append.restype = i
+        lib.csr_oracle_rope.argtypes = [p, p, ctypes.c_int64, i, i, i, d, p]
+        lib.csr_oracle_rope.restype = i
         _lib = lib
     return _lib
 
@@ -55,16 +59,47 @@ def default_threads() -> int:
     return len(os.sched_getaffinity(0))
 
 
+def _rope_args(rope, head_dim):
+    """``rope`` = None or ``(style, rotary_dims, base)``; rotary_dims 0 means all."""
+    if rope is None or rope[0] == ROPE_NONE:
+        return ROPE_NONE, 0, 0.0
+    style, r, base = rope
+    return int(style), int(r or head_dim), float(base)
+
+
+def rope(x, positions, style, rotary_dims, base):
+    """RoFormer's rotary position embedding (Su et al., 2021) of fp64 rows
+    ``x [R, d]`` (or ``[R, H, d]``, one position per leading row) at
+    ``positions [R]``: pair i of the first ``rotary_dims`` dims turns by
+    ``position * base**(-2i/rotary_dims)``; ``style`` picks the pairing
+    (ROPE_NEOX: i with i + r/2, ROPE_INTERLEAVED: 2i with 2i + 1)."""
+    lib = _load()
+    x = np.ascontiguousarray(x, dtype=np.float64)
+    R = x.shape[0]
+    d = x.shape[-1]
+    per = int(np.prod(x.shape[1:-1])) if x.ndim > 2 else 1
+    pos = np.repeat(np.ascontiguousarray(positions, dtype=np.int64).reshape(R), per)
+    y = np.empty_like(x)
+    rc = lib.csr_oracle_rope(_ptr(x), _ptr(y), R * per, d, int(rotary_dims or d), int(style), float(base),
+                             _ptr(pos))
+    if rc != 0:
+        raise ValueError("malformed rotary embedding arguments")
+    return y
+
+
 def attention(dtype, q, k_new, v_new, k_pool, v_pool, block_table, bt_stride, cu_seqlens_q,
               cache_len, rows, num_q_heads, num_kv_heads, head_dim, page_size, scale=None,
-              nthreads=None):
+              nthreads=None, rope=None):
     """Extend attention for the query tokens in ``rows`` (all heads).
 
     Paper Sec. II, eq. (causal_attention_1)-(causal_attention_3) over the
     cached concatenation of eq. (K_cache)-(V_cache); prefix length L_b = i* - 1
     (eq. (csr_i_star)).  ``cache_len=None`` is the L_b = 0 full re-prefill
     (warm-up of Algorithm 1).  Arrays: bf16 as uint16 bit patterns, fp32 as
-    float32.  Returns ``(out [R,Hq,d] f64, lse [R,Hq] f64, pairs [R,Hq] i64)``.
+    float32.  ``rope=(style, rotary_dims, base)`` first rotates every query
+    row and every chunk key at its absolute position (see ``rope``); cached
+    keys are used as stored.  Returns ``(out [R,Hq,d] f64, lse [R,Hq] f64,
+    pairs [R,Hq] i64)``.
     """
     lib = _load()
     G = num_q_heads // num_kv_heads
@@ -81,7 +116,7 @@ def attention(dtype, q, k_new, v_new, k_pool, v_pool, block_table, bt_stride, cu
     cl = _i32(cache_len)
     rc = lib.csr_oracle_attention(
         dtype, num_q_heads, num_kv_heads, head_dim, page_size, 0.0 if scale is None else float(scale),
-        int(cu.shape[0] - 1), *[_ptr(a) for a in arrs], _ptr(bt), int(bt_stride), _ptr(cu), _ptr(cl),
+        *_rope_args(rope, head_dim), int(cu.shape[0] - 1), *[_ptr(a) for a in arrs], _ptr(bt), int(bt_stride), _ptr(cu), _ptr(cl),
         R, _ptr(rows), _ptr(out), _ptr(lse), _ptr(pairs), int(nthreads or default_threads()))
     if rc != 0:
         raise RuntimeError(f"oracle attention failed ({rc})")
@@ -89,9 +124,11 @@ def attention(dtype, q, k_new, v_new, k_pool, v_pool, block_table, bt_stride, cu
 
 
 def kv_append(k_new, v_new, k_pool, v_pool, block_table, bt_stride, cu_seqlens_q, cache_len,
-              num_kv_heads, head_dim, page_size):
+              num_kv_heads, head_dim, page_size, rope=None):
     """Append oracle, in place on copies: Theorem 2's T (+) dX as a bit copy of
-    each chunk row into cache position L_b + i.  Returns the new pools."""
+    each chunk row into cache position L_b + i.  With ``rope`` the key rows are
+    rotated at that position and rounded to the pool's type (nearest, ties to
+    even) instead.  bf16 as uint16 bit patterns.  Returns the new pools."""
     lib = _load()
     kp = np.array(k_pool, copy=True)
     vp = np.array(v_pool, copy=True)
@@ -100,7 +137,9 @@ def kv_append(k_new, v_new, k_pool, v_pool, block_table, bt_stride, cu_seqlens_q
     bt = _i32(block_table)
     cu = _i32(cu_seqlens_q)
     cl = _i32(cache_len)
-    rc = lib.csr_oracle_kv_append(kn.itemsize, num_kv_heads, head_dim, page_size, int(cu.shape[0] - 1),
+    dt = {np.dtype(np.uint16): BF16, np.dtype(np.float32): F32}[kn.dtype]
+    rc = lib.csr_oracle_kv_append(dt, num_kv_heads, head_dim, page_size, *_rope_args(rope, head_dim),
+                                  int(cu.shape[0] - 1),
                                   _ptr(kn), _ptr(vn), _ptr(kp), _ptr(vp), _ptr(bt), int(bt_stride),
                                   _ptr(cu), _ptr(cl))
     if rc != 0:
