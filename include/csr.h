@@ -17,6 +17,19 @@
  * re-prefill that asynchronous state reconciliation runs at eviction
  * (Algorithm 1, warm-up; Theorem 4).
  *
+ * Rotary position embedding (optional, csr_attn_desc.rope_style): the paper's
+ * q_n and k_n are the projections of the token at position n; models of the
+ * family it deploys rotate both at that position first (RoFormer, Su et al.
+ * 2021).  With rope_style set, the library applies the rotation itself at the
+ * absolute cache position L_b + i of each chunk row, to q and k_new, before the
+ * attention and before the append, so a cached key is rotated exactly once and
+ * never moves again (prefix stability, Theorem 1).  The first r = rope_dim dims
+ * form r/2 pairs; pair i turns by pos * rope_theta^(-2i/r); CSR_ROPE_NEOX pairs
+ * dim i with dim i + r/2, CSR_ROPE_INTERLEAVED pairs dim 2i with dim 2i + 1;
+ * dims >= r pass through.  Rotated values are computed in fp32 (angles reduced
+ * in fp64) and rounded to the element type (nearest, ties to even).  Keys that
+ * are already in the cache are read as stored.
+ *
  * Memory layout (all row-major, element type per csr_attn_desc.dtype):
  *   q                 [T_q][Hq][d]        T_q = cu_seqlens_q[batch]
  *   k_new, v_new      [T_q][Hkv][d]
@@ -68,6 +81,13 @@ typedef enum { CSR_F32 = 0, CSR_BF16 = 1 } csr_dtype;
 /* csr_extend_attention flags */
 #define CSR_APPEND 1u /* also append the chunk's K/V to the cache (csr_kv_append) */
 
+/* csr_attn_desc.rope_style */
+typedef enum {
+  CSR_ROPE_NONE = 0,        /* q and k arrive already carrying their positions */
+  CSR_ROPE_NEOX = 1,        /* pairs (i, i + r/2) */
+  CSR_ROPE_INTERLEAVED = 2  /* pairs (2i, 2i + 1) */
+} csr_rope_style;
+
 /* Attention geometry shared by every call. */
 typedef struct {
   int32_t num_q_heads;   /* Hq >= 1 */
@@ -76,6 +96,9 @@ typedef struct {
   int32_t page_size;     /* P: power of two, 1 .. 1024 */
   float softmax_scale;   /* > 0, or 0 for 1/sqrt(d) (the paper's 1/sqrt(d_k)) */
   int32_t dtype;         /* csr_dtype: CSR_BF16 (fp32 accumulate) or CSR_F32 */
+  int32_t rope_style;    /* csr_rope_style; 0 (all fields zero) = no rotation */
+  int32_t rope_dim;      /* r: rotated leading dims, a multiple of 16 in [16, d]; 0 = d */
+  float rope_theta;      /* base of the pair frequencies, finite and > 0 (e.g. 1e4, 1e6) */
 } csr_attn_desc;
 
 /*
@@ -84,7 +107,10 @@ typedef struct {
  * (incremental_extensibility)).  Chunk row i of sequence b (row
  * cu_seqlens_q[b] + i of k_new / v_new) is copied bit for bit to cache
  * position L_b + i, for every kv head.  No other byte of either pool changes,
- * so every cached position < L_b stays as it was.  Committing the appended
+ * so every cached position < L_b stays as it was.  With desc->rope_style set,
+ * each key row is rotated at its position L_b + i and rounded to the element
+ * type instead of copied (values are still copied bit for bit); the pass is
+ * fused into the same launch.  Committing the appended
  * rows (advancing L_b) is the caller's choice: rows of the dynamic suffix are
  * simply overwritten by the next call.
  *   cu_seqlens_q   [batch+1] device int32 prefix sums of n_b
@@ -100,8 +126,11 @@ csr_status csr_kv_append(const csr_attn_desc* desc, int32_t batch, const void* k
                          int32_t total_q, void* stream);
 
 /*
- * Workspace bytes csr_extend_attention needs for these sizes (0 when the plan
- * uses no split-K).  The same host integers must be passed to the call.
+ * Workspace bytes csr_extend_attention needs for these sizes: split-K
+ * partials when the plan splits the key range, plus rotated copies of q and
+ * k_new ([T_q][Hq][d] and [T_q][Hkv][d], 256-byte aligned) when
+ * desc->rope_style is set; 0 when neither applies.  The same host integers
+ * must be passed to the call.
  */
 size_t csr_extend_workspace_size(const csr_attn_desc* desc, int32_t batch, int32_t total_q,
                                  int32_t max_seqlen_q, int32_t max_cache_len);
@@ -115,7 +144,12 @@ size_t csr_extend_workspace_size(const csr_attn_desc* desc, int32_t batch, int32
  *                     of L_b (they size the launch; exceeding them is an error
  *                     the library cannot detect)
  *   flags             CSR_APPEND: enqueue csr_kv_append first (the attention
- *                     itself reads chunk keys from k_new / v_new either way)
+ *                     itself reads chunk keys from k_new / v_new either way,
+ *                     or from their rotated workspace copies with RoPE)
+ *   q, k_new          with desc->rope_style set: unrotated projections; one
+ *                     fused launch writes their rotations at L_b + i to the
+ *                     workspace (and, with CSR_APPEND, the rotated keys and
+ *                     the values to the cache) before the attention
  *   out               [T_q][Hq][d], element type of q
  *   lse               [T_q][Hq] float or NULL
  *   workspace         device scratch of >= csr_extend_workspace_size() bytes
@@ -131,7 +165,7 @@ csr_status csr_extend_attention(const csr_attn_desc* desc, int32_t batch, const 
                                 uint32_t flags, void* out, float* lse, void* workspace,
                                 size_t workspace_bytes, void* stream);
 
-/* Workspace bytes csr_prefill needs (0 when the plan uses no split-K). */
+/* Workspace bytes csr_prefill needs (split-K partials, rotated q/k with RoPE; 0 if neither). */
 size_t csr_prefill_workspace_size(const csr_attn_desc* desc, int32_t batch, int32_t total,
                                   int32_t max_seqlen);
 
@@ -142,6 +176,8 @@ size_t csr_prefill_workspace_size(const csr_attn_desc* desc, int32_t batch, int3
  * Same computation as csr_extend_attention with no cached prefix.  If k_pool
  * is non-NULL the sequence's K/V are also written to the cache at positions
  * 0 .. n_b - 1 (the warmed-up cache), exactly as csr_kv_append with L_b = 0.
+ * With desc->rope_style set, q and k are rotated at positions 0 .. n_b - 1
+ * (the workspace then also holds the rotated copies, as for extend).
  */
 csr_status csr_prefill(const csr_attn_desc* desc, int32_t batch, const void* q, const void* k,
                        const void* v, void* k_pool, void* v_pool, int32_t num_pages,

@@ -53,10 +53,64 @@ csr_status check_desc(const csr_attn_desc* d) {
     return fail(CSR_E_INVAL, "page_size %d must be a power of two in [1, 1024]", d->page_size);
   if (!(d->softmax_scale >= 0.f) || isinf(d->softmax_scale))
     return fail(CSR_E_INVAL, "softmax_scale must be finite and >= 0 (0 = 1/sqrt(d))");
+  if (d->rope_style != CSR_ROPE_NONE) {
+    if (d->rope_style != CSR_ROPE_NEOX && d->rope_style != CSR_ROPE_INTERLEAVED)
+      return fail(CSR_E_INVAL, "unknown rope_style %d", d->rope_style);
+    const int r = d->rope_dim ? d->rope_dim : d->head_dim;
+    if (r < 16 || r > d->head_dim || r % 16)
+      return fail(CSR_E_UNSUPPORTED, "rope_dim %d must be a multiple of 16 in [16, head_dim=%d]", d->rope_dim,
+                  d->head_dim);
+    if (!(d->rope_theta > 0.f) || isinf(d->rope_theta))
+      return fail(CSR_E_INVAL, "rope_theta must be finite and > 0");
+  }
   return CSR_OK;
 }
 
+bool has_rope(const csr_attn_desc* d) { return d->rope_style != CSR_ROPE_NONE; }
+
+size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
+
 int elem_bytes(const csr_attn_desc* d) { return d->dtype == CSR_BF16 ? 2 : 4; }
+
+// Workspace head used by RoPE: rotated q, then rotated k (each 256-aligned).
+size_t rope_q_bytes(const csr_attn_desc* d, int total) {
+  return align256((size_t)total * d->num_q_heads * d->head_dim * elem_bytes(d));
+}
+size_t rope_ws_bytes(const csr_attn_desc* d, int total) {
+  if (!has_rope(d)) return 0;
+  return rope_q_bytes(d, total) + align256((size_t)total * d->num_kv_heads * d->head_dim * elem_bytes(d));
+}
+
+// q / q_out may be NULL (keys only), k_pool NULL (no cache write).
+csr::RopeArgs rope_args(const csr_attn_desc* d, int batch, const void* q, const void* k, const void* v, void* q_out,
+                        void* k_out, void* k_pool, void* v_pool, int num_pages, const int32_t* bt, int bt_stride,
+                        const int32_t* cu, const int32_t* cache_len, int total) {
+  csr::RopeArgs a;
+  a.q = q;
+  a.k = k;
+  a.v = v;
+  a.q_out = q_out;
+  a.k_out = k_out;
+  a.k_pool = k_pool;
+  a.v_pool = v_pool;
+  a.block_table = bt;
+  a.cu_q = cu;
+  a.cache_len = cache_len;
+  a.num_pages = num_pages;
+  a.bt_stride = bt_stride;
+  a.batch = batch;
+  a.total_q = total;
+  a.Hq = d->num_q_heads;
+  a.Hkv = d->num_kv_heads;
+  a.d = d->head_dim;
+  a.log2P = ilog2(d->page_size);
+  a.rdim = d->rope_dim ? d->rope_dim : d->head_dim;
+  a.style = d->rope_style;
+  // Pair i turns by pos * theta^(-2i/r) radians: store that rate in half-turns.
+  for (int i = 0; i < 64; ++i)
+    a.half_turns[i] = i < a.rdim / 2 ? pow((double)d->rope_theta, -2.0 * i / a.rdim) / M_PI : 0.0;
+  return a;
+}
 
 // Launch plan: row tiles, key splits, workspace.  Pure function of the host
 // integers and the device's CU count, so the size query and the call agree.
@@ -274,6 +328,12 @@ csr_status csr_kv_append(const csr_attn_desc* desc, int32_t batch, const void* k
   st = check_pool(desc, k_pool, v_pool, num_pages, block_table, bt_stride, 0, "kv_append");
   if (st != CSR_OK) return st;
   if (cache_seqlens && !aligned4(cache_seqlens)) return fail(CSR_E_INVAL, "cache_seqlens must be 4-byte aligned");
+  if (has_rope(desc)) {
+    const csr::RopeArgs r = rope_args(desc, batch, nullptr, k_new, v_new, nullptr, nullptr, k_pool, v_pool,
+                                      num_pages, block_table, bt_stride, cu_seqlens_q, cache_seqlens, total_q);
+    return launched(csr::launch_rope_append(r, desc->dtype == CSR_BF16, static_cast<hipStream_t>(stream)),
+                    "rope kv_append");
+  }
   const csr::AppendArgs a = append_args(desc, batch, k_new, v_new, k_pool, v_pool, num_pages, block_table, bt_stride,
                                         cu_seqlens_q, cache_seqlens, total_q);
   return launched(csr::launch_append(a, static_cast<hipStream_t>(stream)), "kv_append");
@@ -284,7 +344,7 @@ size_t csr_extend_workspace_size(const csr_attn_desc* desc, int32_t batch, int32
   if (check_desc(desc) != CSR_OK || batch < 1 || total_q < 1 || max_seqlen_q < 1 || max_cache_len < 0) return 0;
   Plan p;
   if (make_plan(desc, batch, total_q, max_seqlen_q, max_cache_len, p) != CSR_OK) return 0;
-  return p.ws_bytes;
+  return rope_ws_bytes(desc, total_q) + p.ws_bytes;
 }
 
 size_t csr_prefill_workspace_size(const csr_attn_desc* desc, int32_t batch, int32_t total, int32_t max_seqlen) {
@@ -316,16 +376,37 @@ csr_status csr_extend_attention(const csr_attn_desc* desc, int32_t batch, const 
     return fail(CSR_E_INVAL, "cache_seqlens must be non-NULL when max_cache_len > 0");
   if (cache_seqlens && !aligned4(cache_seqlens)) return fail(CSR_E_INVAL, "cache_seqlens must be 4-byte aligned");
   hipStream_t s = static_cast<hipStream_t>(stream);
-  if (flags & CSR_APPEND) {
+  // Validate the plan (workspace) before enqueuing anything.
+  Plan p;
+  st = make_plan(desc, batch, total_q, max_seqlen_q, max_cache_len, p);
+  if (st != CSR_OK) return st;
+  const size_t rope_bytes = rope_ws_bytes(desc, total_q);
+  if (rope_bytes + p.ws_bytes > 0) {
+    if (!workspace || workspace_bytes < rope_bytes + p.ws_bytes)
+      return fail(CSR_E_WORKSPACE, "workspace of %zu bytes required, got %zu", rope_bytes + p.ws_bytes,
+                  workspace ? workspace_bytes : (size_t)0);
+    if (!aligned16(workspace)) return fail(CSR_E_INVAL, "workspace must be 16-byte aligned");
+  }
+  const bool append = (flags & CSR_APPEND) != 0;
+  if (rope_bytes > 0) {
+    // Rotate q and k_new at L_b + i into the workspace (and append) in one launch,
+    // then attend over the rotated copies.
+    char* ws = static_cast<char*>(workspace);
+    void* q_rot = ws;
+    void* k_rot = ws + rope_q_bytes(desc, total_q);
+    const csr::RopeArgs r = rope_args(desc, batch, q, k_new, v_new, q_rot, k_rot, append ? k_pool : nullptr,
+                                      append ? v_pool : nullptr, num_pages, block_table, bt_stride, cu_seqlens_q,
+                                      cache_seqlens, total_q);
+    st = launched(csr::launch_rope_append(r, desc->dtype == CSR_BF16, s), "rope");
+    if (st != CSR_OK) return st;
+    return run_attention(desc, batch, q_rot, k_rot, v_new, k_pool, v_pool, num_pages, block_table, bt_stride,
+                         cu_seqlens_q, max_cache_len > 0 ? cache_seqlens : nullptr, total_q, max_seqlen_q,
+                         max_cache_len, out, lse, p.ws_bytes ? ws + rope_bytes : nullptr, workspace_bytes - rope_bytes,
+                         s);
+  }
+  if (append) {
     const csr::AppendArgs a = append_args(desc, batch, k_new, v_new, k_pool, v_pool, num_pages, block_table,
                                           bt_stride, cu_seqlens_q, cache_seqlens, total_q);
-    // Validate the plan (workspace) before enqueuing anything.
-    Plan p;
-    st = make_plan(desc, batch, total_q, max_seqlen_q, max_cache_len, p);
-    if (st != CSR_OK) return st;
-    if (p.ws_bytes > 0 && (!workspace || workspace_bytes < p.ws_bytes))
-      return fail(CSR_E_WORKSPACE, "workspace of %zu bytes required, got %zu", p.ws_bytes,
-                  workspace ? workspace_bytes : (size_t)0);
     st = launched(csr::launch_append(a, s), "kv_append");
     if (st != CSR_OK) return st;
   }
@@ -350,10 +431,27 @@ csr_status csr_prefill(const csr_attn_desc* desc, int32_t batch, const void* q, 
   Plan p;
   st = make_plan(desc, batch, total, max_seqlen, 0, p);
   if (st != CSR_OK) return st;
-  if (p.ws_bytes > 0 && (!workspace || workspace_bytes < p.ws_bytes))
-    return fail(CSR_E_WORKSPACE, "workspace of %zu bytes required, got %zu", p.ws_bytes,
-                workspace ? workspace_bytes : (size_t)0);
+  const size_t rope_bytes = rope_ws_bytes(desc, total);
+  if (rope_bytes + p.ws_bytes > 0) {
+    if (!workspace || workspace_bytes < rope_bytes + p.ws_bytes)
+      return fail(CSR_E_WORKSPACE, "workspace of %zu bytes required, got %zu", rope_bytes + p.ws_bytes,
+                  workspace ? workspace_bytes : (size_t)0);
+    if (!aligned16(workspace)) return fail(CSR_E_INVAL, "workspace must be 16-byte aligned");
+  }
   hipStream_t s = static_cast<hipStream_t>(stream);
+  if (rope_bytes > 0) {
+    char* ws = static_cast<char*>(workspace);
+    void* q_rot = ws;
+    void* k_rot = ws + rope_q_bytes(desc, total);
+    const csr::RopeArgs r = rope_args(desc, batch, q, k, v, q_rot, k_rot, write_cache ? k_pool : nullptr,
+                                      write_cache ? v_pool : nullptr, num_pages, block_table, bt_stride, cu_seqlens,
+                                      nullptr, total);
+    st = launched(csr::launch_rope_append(r, desc->dtype == CSR_BF16, s), "rope");
+    if (st != CSR_OK) return st;
+    return run_attention(desc, batch, q_rot, k_rot, v, nullptr, nullptr, 0, nullptr, 1, cu_seqlens, nullptr, total,
+                         max_seqlen, 0, out, lse, p.ws_bytes ? ws + rope_bytes : nullptr, workspace_bytes - rope_bytes,
+                         s);
+  }
   if (write_cache) {
     const csr::AppendArgs a = append_args(desc, batch, k, v, k_pool, v_pool, num_pages, block_table, bt_stride,
                                           cu_seqlens, nullptr, total);

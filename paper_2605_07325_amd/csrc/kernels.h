@@ -58,4 +58,23 @@ struct AppendArgs {
 };
 hipError_t launch_append(const AppendArgs& a, hipStream_t stream);
 
+// Rotary embedding at absolute positions L_b + i, fused with the append.
+struct RopeArgs {
+  const void* q;             // [T_q][Hq][d] or nullptr (keys only)
+  const void* k;             // [T_q][Hkv][d]
+  const void* v;             // [T_q][Hkv][d], read only when k_pool is set
+  void* q_out;               // rotated q, or nullptr
+  void* k_out;               // rotated k, or nullptr
+  void* k_pool;              // nullptr: no cache write
+  void* v_pool;
+  const int32_t* block_table;
+  const int32_t* cu_q;
+  const int32_t* cache_len;  // nullptr: every L_b = 0
+  int32_t num_pages, bt_stride, batch, total_q, Hq, Hkv, d, log2P;
+  int32_t rdim;              // rotated dims, multiple of 16, <= d
+  int32_t style;             // 1 neox (i, i + r/2), 2 interleaved (2i, 2i + 1)
+  double half_turns[64];     // theta_i / pi for i < rdim / 2
+};
+hipError_t launch_rope_append(const RopeArgs& a, int dtype_bf16, hipStream_t stream);
+
 }  // namespace csr

@@ -1,0 +1,192 @@
+// Rotary position embedding (RoFormer, Su et al. 2021) at absolute cache
+// positions, fused with the paged KV append.
+//
+// Chunk row i of sequence b sits at position pos = L_b + i, fixed for as long
+// as the row stays cached (prefix stability, Theorem 1), so its query and key
+// are rotated once, here, and the rotated key is what the cache keeps
+// (append-only growth, Theorem 2).
+//
+// One workgroup per token.  The token's sequence and position are uniform over
+// the workgroup.  The first r/2 threads form (cos, sin) of each pair angle
+// pos * theta_i into LDS: the angle is reduced to half-turns in [-1, 1] in
+// fp64 (pos * theta_i / pi, minus the nearest even integer), then sincospif
+// evaluates it in fp32, so the phase error stays ~1e-7 rad even at positions
+// near 2^17 where a plain fp32 product would be off by ~1e-2 rad.  Every
+// thread then takes 8-element pieces of the token's rows: a neox piece rotates
+// elements [e, e+8) against [e + r/2, e + r/2 + 8), an interleaved piece
+// rotates the four pairs inside [e, e+8), tail pieces (dims >= r) and value
+// rows are copied bit for bit.  Loads and stores are 16 bytes per lane, and
+// consecutive lanes take consecutive pieces of a row.
+#include "kernels.h"
+
+namespace csr {
+
+namespace {
+
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+typedef float f32x2 __attribute__((ext_vector_type(2)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+
+__device__ __forceinline__ int token_sequence(const int32_t* __restrict__ cu, int batch, int tok) {
+  int lo = 0, hi = batch - 1;  // largest b with cu[b] <= tok
+  while (lo < hi) {
+    const int mid = (lo + hi + 1) >> 1;
+    if (cu[mid] <= tok) lo = mid; else hi = mid - 1;
+  }
+  return lo;
+}
+
+__device__ __forceinline__ float lo_bf16(uint32_t w) { return __builtin_bit_cast(float, w << 16); }
+__device__ __forceinline__ float hi_bf16(uint32_t w) { return __builtin_bit_cast(float, w & 0xffff0000u); }
+__device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
+  f32x2 f = {lo, hi};
+  return __builtin_bit_cast(uint32_t, __builtin_convertvector(f, bf16x2));  // nearest, ties to even
+}
+
+// 8 consecutive elements as floats (BF16: one 16-byte load; fp32: two).
+template <bool BF16>
+__device__ __forceinline__ void load8(const void* base, int64_t e, float (&x)[8]) {
+  if constexpr (BF16) {
+    const u32x4 w = *reinterpret_cast<const u32x4*>(static_cast<const uint16_t*>(base) + e);
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      x[2 * j] = lo_bf16(w[j]);
+      x[2 * j + 1] = hi_bf16(w[j]);
+    }
+  } else {
+    // Loaded as float vectors: a bit cast of one element of an integer vector
+    // would read element 0 (clang lowers it through the vector's address).
+    const f32x4* p = reinterpret_cast<const f32x4*>(static_cast<const float*>(base) + e);
+    const f32x4 a = p[0], b = p[1];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      x[j] = a[j];
+      x[4 + j] = b[j];
+    }
+  }
+}
+
+template <bool BF16>
+__device__ __forceinline__ void store8(void* base, int64_t e, const float (&y)[8]) {
+  if constexpr (BF16) {
+    const u32x4 w = {pack_bf16x2(y[0], y[1]), pack_bf16x2(y[2], y[3]), pack_bf16x2(y[4], y[5]),
+                     pack_bf16x2(y[6], y[7])};
+    *reinterpret_cast<u32x4*>(static_cast<uint16_t*>(base) + e) = w;
+  } else {
+    f32x4* p = reinterpret_cast<f32x4*>(static_cast<float*>(base) + e);
+    p[0] = f32x4{y[0], y[1], y[2], y[3]};
+    p[1] = f32x4{y[4], y[5], y[6], y[7]};
+  }
+}
+
+// Bit copy of 8 elements (tail dims, value rows).
+template <bool BF16>
+__device__ __forceinline__ void copy8(void* dst, const void* src, int64_t de, int64_t se) {
+  constexpr int kWords = BF16 ? 1 : 2;
+  const u32x4* s = reinterpret_cast<const u32x4*>(static_cast<const char*>(src) + se * (BF16 ? 2 : 4));
+  u32x4* d = reinterpret_cast<u32x4*>(static_cast<char*>(dst) + de * (BF16 ? 2 : 4));
+#pragma unroll
+  for (int j = 0; j < kWords; ++j) d[j] = s[j];
+}
+
+template <bool BF16>
+__global__ void __launch_bounds__(256) rope_append_kernel(RopeArgs a) {
+  __shared__ f32x2 cs[64];
+  const int tok = blockIdx.x;
+  const int b = token_sequence(a.cu_q, a.batch, tok);
+  const int64_t pos = (int64_t)(a.cache_len ? a.cache_len[b] : 0) + (tok - a.cu_q[b]);
+  const int half = a.rdim >> 1;
+  if ((int)threadIdx.x < half) {
+    double t = (double)pos * a.half_turns[threadIdx.x];  // angle / pi
+    t -= 2.0 * rint(0.5 * t);                             // same angle, now in [-1, 1]
+    float s, c;
+    sincospif((float)t, &s, &c);
+    cs[threadIdx.x] = f32x2{c, s};
+  }
+
+  // Cache slot of this token (pool writes only); an invalid page drops them.
+  int64_t slot = -1;
+  if (a.k_pool) {
+    const int64_t pidx = pos >> a.log2P;
+    const int64_t page = a.block_table ? (int64_t)a.block_table[(int64_t)b * a.bt_stride + pidx]
+                                       : (int64_t)b * a.bt_stride + pidx;
+    if (page >= 0 && page < a.num_pages) slot = (page << a.log2P) + (pos & ((1 << a.log2P) - 1));
+  }
+  __syncthreads();
+
+  const int d = a.d;
+  const bool neox = a.style == 1;
+  const int n_rot = neox ? a.rdim >> 4 : a.rdim >> 3;  // rotating pieces per row
+  const int per_row = n_rot + ((d - a.rdim) >> 3);      // + tail pieces
+  const int nq = a.q ? a.Hq : 0;
+  const int rows = nq + a.Hkv;
+  const int rot_units = rows * per_row;
+  const int v_units = slot >= 0 ? a.Hkv * (d >> 3) : 0;
+
+  for (int u = threadIdx.x; u < rot_units + v_units; u += blockDim.x) {
+    if (u >= rot_units) {  // value row piece: bit copy into the cache
+      const int w = u - rot_units;
+      const int g = w / (d >> 3), e = (w - g * (d >> 3)) << 3;
+      copy8<BF16>(a.v_pool, a.v, (slot * a.Hkv + g) * d + e, ((int64_t)tok * a.Hkv + g) * d + e);
+      continue;
+    }
+    const int r = u / per_row, piece = u - r * per_row;
+    const bool is_q = r < nq;
+    const int h = is_q ? r : r - nq;
+    const void* src = is_q ? a.q : a.k;
+    const int64_t row = ((int64_t)tok * (is_q ? a.Hq : a.Hkv) + h) * d;
+    void* out = is_q ? a.q_out : a.k_out;
+    void* pool = is_q ? nullptr : (slot >= 0 ? a.k_pool : nullptr);
+    const int64_t prow = is_q ? 0 : (slot * a.Hkv + h) * d;
+    if (piece >= n_rot) {  // dims >= r: unchanged
+      const int e = a.rdim + ((piece - n_rot) << 3);
+      if (out) copy8<BF16>(out, src, row + e, row + e);
+      if (pool) copy8<BF16>(pool, src, prow + e, row + e);
+      continue;
+    }
+    if (neox) {
+      const int e0 = piece << 3, e1 = e0 + half;
+      float x0[8], x1[8], y0[8], y1[8];
+      load8<BF16>(src, row + e0, x0);
+      load8<BF16>(src, row + e1, x1);
+#pragma unroll
+      for (int j = 0; j < 8; ++j) {
+        const f32x2 t = cs[e0 + j];
+        y0[j] = fmaf(x0[j], t[0], -x1[j] * t[1]);
+        y1[j] = fmaf(x1[j], t[0], x0[j] * t[1]);
+      }
+      if (out) {
+        store8<BF16>(out, row + e0, y0);
+        store8<BF16>(out, row + e1, y1);
+      }
+      if (pool) {
+        store8<BF16>(pool, prow + e0, y0);
+        store8<BF16>(pool, prow + e1, y1);
+      }
+    } else {
+      const int e0 = piece << 3;
+      float x[8], y[8];
+      load8<BF16>(src, row + e0, x);
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const f32x2 t = cs[(e0 >> 1) + j];
+        y[2 * j] = fmaf(x[2 * j], t[0], -x[2 * j + 1] * t[1]);
+        y[2 * j + 1] = fmaf(x[2 * j + 1], t[0], x[2 * j] * t[1]);
+      }
+      if (out) store8<BF16>(out, row + e0, y);
+      if (pool) store8<BF16>(pool, prow + e0, y);
+    }
+  }
+}
+
+}  // namespace
+
+hipError_t launch_rope_append(const RopeArgs& a, int dtype_bf16, hipStream_t stream) {
+  if (a.total_q == 0) return hipSuccess;
+  if (dtype_bf16) hipLaunchKernelGGL(rope_append_kernel<true>, dim3((unsigned)a.total_q), dim3(256), 0, stream, a);
+  else hipLaunchKernelGGL(rope_append_kernel<false>, dim3((unsigned)a.total_q), dim3(256), 0, stream, a);
+  return hipGetLastError();
+}
+
+}  // namespace csr

@@ -143,3 +143,33 @@ def test_event_hook_requires_both_events():
     lib = csr.lib()
     assert lib.csr_set_attention_events(ctypes.c_void_p(FAKE), None) == csr.CSR_E_INVAL
     assert lib.csr_set_attention_events(None, None) == csr.CSR_OK
+
+
+@pytest.mark.parametrize("over,code", [
+    (dict(rope_style=3, rope_theta=1e4), csr.CSR_E_INVAL),                 # unknown pairing
+    (dict(rope_style=csr.CSR_ROPE_NEOX, rope_theta=0.0), csr.CSR_E_INVAL),  # no base
+    (dict(rope_style=csr.CSR_ROPE_NEOX, rope_theta=float("inf")), csr.CSR_E_INVAL),
+    (dict(rope_style=csr.CSR_ROPE_NEOX, rope_theta=float("nan")), csr.CSR_E_INVAL),
+    (dict(rope_style=csr.CSR_ROPE_NEOX, rope_dim=24, rope_theta=1e4), csr.CSR_E_UNSUPPORTED),   # not a multiple of 16
+    (dict(rope_style=csr.CSR_ROPE_INTERLEAVED, rope_dim=144, rope_theta=1e4), csr.CSR_E_UNSUPPORTED),  # > d
+])
+def test_rope_descriptor_validation(over, code):
+    assert call_extend(good_desc(**over)) == code
+    assert csr.lib().csr_last_error().decode()
+
+
+def test_rope_workspace_holds_rotated_q_and_k():
+    plain = good_desc(num_q_heads=64, num_kv_heads=4)
+    rope = good_desc(num_q_heads=64, num_kv_heads=4, rope_style=csr.CSR_ROPE_NEOX, rope_theta=1e6)
+    for T, L in ((512, 122880), (8, 0), (3, 100)):
+        extra = csr.extend_workspace_size(rope, 1, T, T, L) - csr.extend_workspace_size(plain, 1, T, T, L)
+        align = lambda x: (x + 255) // 256 * 256  # noqa: E731
+        assert extra == align(T * 64 * 128 * 2) + align(T * 4 * 128 * 2)
+    # prefill needs them too, and a call with too small a workspace is refused before any launch
+    assert csr.prefill_workspace_size(rope, 1, 8, 8) >= align(8 * 64 * 128 * 2) + align(8 * 4 * 128 * 2)
+    need = csr.extend_workspace_size(rope, 1, 16, 16, 100)
+    st = call_extend(good_desc(rope_style=csr.CSR_ROPE_NEOX, rope_theta=1e4), ws=FAKE,
+                     ws_bytes=csr.extend_workspace_size(good_desc(rope_style=csr.CSR_ROPE_NEOX, rope_theta=1e4), 1, 16,
+                                                        16, 100) - 16)
+    assert need > 0 and st == csr.CSR_E_WORKSPACE
+    assert call_extend(good_desc(rope_style=csr.CSR_ROPE_NEOX, rope_theta=1e4), ws=None) == csr.CSR_E_WORKSPACE
