@@ -14,7 +14,14 @@ synchronisations, timed with events on the stream the library launches on.
 Consecutive steps read different copies of the K/V pool (three copies of about
 250 MB), so the 256 MB Infinity Cache cannot serve a step's prefix from the
 previous step.  The attention kernel's own duration is read live through the
-library's csr_set_attention_events hook.
+library's csr_set_attention_events hook.  Each event record leaves a gap of a
+few microseconds between launches, so the same steps are timed once more
+without the hook (``ms_per_step_without_event_hook``); for the short decode
+steps the difference is visible, for the 512-token chunk it is below 1 %.
+
+``--rope neox|interleaved`` rotates q and k_new at their absolute positions
+inside the step (one fused rotate-and-append launch before the attention) and
+reports the hook-free step time with and without the rotation.
 
 Prints one JSON line.  ``--gpus N`` with N > 1 is rejected: this build runs
 on one GPU.
@@ -135,6 +142,10 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--no-prefill-ratio", action="store_true")
+    ap.add_argument("--rope", choices=("none", "neox", "interleaved"), default="none",
+                    help="rotate q and k_new at their absolute positions inside the step (fused with the append)")
+    ap.add_argument("--rope-theta", type=float, default=1e6)
+    ap.add_argument("--rope-dim", type=int, default=0, help="rotated dims (0 = head_dim)")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="also run a 1 GiB device copy (HBM counter calibration for rocprofv3 --pmc runs)")
     args = ap.parse_args()
@@ -175,8 +186,12 @@ def main():
     bt = None if case.block_table is None else torch.from_numpy(case.block_table).cuda()
     cu = torch.from_numpy(case.cu_seqlens_q).cuda()
     cl = torch.from_numpy(case.cache_len).cuda()
+    rope_style = {"none": csr.CSR_ROPE_NONE, "neox": csr.CSR_ROPE_NEOX, "interleaved": csr.CSR_ROPE_INTERLEAVED}[args.rope]
+    plain_desc = csr.make_desc(case.num_q_heads, case.num_kv_heads, case.head_dim, case.page_size,
+                               torch.bfloat16 if bf16 else torch.float32)
     desc = csr.make_desc(case.num_q_heads, case.num_kv_heads, case.head_dim, case.page_size,
-                         torch.bfloat16 if bf16 else torch.float32)
+                         torch.bfloat16 if bf16 else torch.float32, rope_style=rope_style, rope_dim=args.rope_dim,
+                         rope_theta=args.rope_theta if rope_style else 0.0)
     out = torch.empty_like(q)
     lse = torch.empty((case.total_q, case.num_q_heads), dtype=torch.float32, device="cuda")
     if prefill_mode:
@@ -185,13 +200,13 @@ def main():
         ws_bytes = csr.extend_workspace_size(desc, case.batch, case.total_q, case.max_seqlen_q, case.max_cache_len)
     ws = torch.empty(max(ws_bytes, 16), dtype=torch.uint8, device="cuda")
 
-    def step(i):
+    def step(i, d=desc):
         kp, vp = pools[i % len(pools)]
         if prefill_mode:
-            csr.prefill(desc, q, k_new, v_new, cu, case.max_seqlen_q, k_pool=kp, v_pool=vp, block_table=bt,
+            csr.prefill(d, q, k_new, v_new, cu, case.max_seqlen_q, k_pool=kp, v_pool=vp, block_table=bt,
                         bt_stride=case.bt_stride, out=out, lse=lse, workspace=ws)
         else:
-            csr.extend_attention(desc, q, k_new, v_new, kp, vp, bt, case.bt_stride, cu, cl, case.max_seqlen_q,
+            csr.extend_attention(d, q, k_new, v_new, kp, vp, bt, case.bt_stride, cu, cl, case.max_seqlen_q,
                                  case.max_cache_len, append=True, out=out, lse=lse, workspace=ws)
 
     if args.copy_calibration:
@@ -272,6 +287,40 @@ def main():
             "hbm_gbs_algorithmic": round(abytes / (attn_avg * 1e-3) / 1e9, 1),
         },
     }
+    def hookless_ms(d):
+        """Step time of the same loop without the event hook (each hipEventRecord
+        between two launches leaves a gap of several microseconds, which matters
+        for the short decode steps)."""
+        for i in range(3):
+            step(i, d)
+        torch.cuda.synchronize()
+        s3, e3 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        s3.record()
+        for i in range(args.steps):
+            step(args.warmup + i, d)
+        e3.record()
+        torch.cuda.synchronize()
+        return s3.elapsed_time(e3) / args.steps
+
+    plain_ms = hookless_ms(desc)
+    rec["ms_per_step_without_event_hook"] = round(plain_ms, 5)
+    log(f"same steps without the attention event hook: {plain_ms:.4f} ms/step")
+    if rope_style:
+        # Same process, same inputs, both without the hook: the step without the rotation.
+        unrotated_ms = hookless_ms(plain_desc)
+        e = case.elem_bytes
+        rope_bytes = case.total_q * case.head_dim * e * (2 * case.num_q_heads + 5 * case.num_kv_heads)
+        rec["config"]["workload"] += f", RoPE {args.rope} (theta {args.rope_theta:g}) fused with the append"
+        rec["rope"] = {
+            "style": args.rope, "theta": args.rope_theta, "rotary_dims": args.rope_dim or case.head_dim,
+            "kernel": "rope_append_kernel",
+            "algorithmic_bytes_per_launch": int(rope_bytes),
+            "step_ms": round(plain_ms, 5),
+            "step_ms_without_rope": round(unrotated_ms, 5),
+            "step_overhead_ms": round(plain_ms - unrotated_ms, 5),
+        }
+        log(f"rope: step {plain_ms:.4f} ms vs {unrotated_ms:.4f} ms without rotation (no event hook in either; "
+            f"{rope_bytes / 1e6:.2f} MB moved by the fused rotate+append launch)")
     if not prefill_mode and not args.no_prefill_ratio and bf16:
         S = int(case.cache_len[0] + case.seqlen_q[0])
         g = torch.Generator(device="cuda")

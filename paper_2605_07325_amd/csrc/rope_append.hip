@@ -6,8 +6,11 @@
 // are rotated once, here, and the rotated key is what the cache keeps
 // (append-only growth, Theorem 2).
 //
-// One workgroup per token.  The token's sequence and position are uniform over
-// the workgroup.  The first r/2 threads form (cos, sin) of each pair angle
+// Grid: x = token, y = slices of that token's 8-element pieces.  Short chunks
+// (decode) spread one token over several workgroups, one piece per thread;
+// long ones use one workgroup per token that loops over its pieces, so the
+// angles are formed once per token.  The token's sequence and position are
+// uniform over the workgroup.  The first r/2 threads form (cos, sin) of each pair angle
 // pos * theta_i into LDS: the angle is reduced to half-turns in [-1, 1] in
 // fp64 (pos * theta_i / pi, minus the nearest even integer), then sincospif
 // evaluates it in fp32, so the phase error stays ~1e-7 rad even at positions
@@ -91,6 +94,65 @@ __device__ __forceinline__ void copy8(void* dst, const void* src, int64_t de, in
 }
 
 template <bool BF16>
+__device__ __forceinline__ void rotate_piece(const RopeArgs& a, const f32x2* cs, int tok, int64_t slot, int u,
+                                             int rot_units, int per_row, int n_rot, int nq, bool neox) {
+  const int d = a.d;
+  const int half = a.rdim >> 1;
+  if (u >= rot_units) {  // value row piece: bit copy into the cache
+    const int w = u - rot_units;
+    const int g = w / (d >> 3), e = (w - g * (d >> 3)) << 3;
+    copy8<BF16>(a.v_pool, a.v, (slot * a.Hkv + g) * d + e, ((int64_t)tok * a.Hkv + g) * d + e);
+    return;
+  }
+  const int r = u / per_row, piece = u - r * per_row;
+  const bool is_q = r < nq;
+  const int h = is_q ? r : r - nq;
+  const void* src = is_q ? a.q : a.k;
+  const int64_t row = ((int64_t)tok * (is_q ? a.Hq : a.Hkv) + h) * d;
+  void* out = is_q ? a.q_out : a.k_out;
+  void* pool = is_q ? nullptr : (slot >= 0 ? a.k_pool : nullptr);
+  const int64_t prow = is_q ? 0 : (slot * a.Hkv + h) * d;
+  if (piece >= n_rot) {  // dims >= r: unchanged
+    const int e = a.rdim + ((piece - n_rot) << 3);
+    if (out) copy8<BF16>(out, src, row + e, row + e);
+    if (pool) copy8<BF16>(pool, src, prow + e, row + e);
+    return;
+  }
+  if (neox) {
+    const int e0 = piece << 3, e1 = e0 + half;
+    float x0[8], x1[8], y0[8], y1[8];
+    load8<BF16>(src, row + e0, x0);
+    load8<BF16>(src, row + e1, x1);
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+      const f32x2 t = cs[e0 + j];
+      y0[j] = fmaf(x0[j], t[0], -x1[j] * t[1]);
+      y1[j] = fmaf(x1[j], t[0], x0[j] * t[1]);
+    }
+    if (out) {
+      store8<BF16>(out, row + e0, y0);
+      store8<BF16>(out, row + e1, y1);
+    }
+    if (pool) {
+      store8<BF16>(pool, prow + e0, y0);
+      store8<BF16>(pool, prow + e1, y1);
+    }
+  } else {
+    const int e0 = piece << 3;
+    float x[8], y[8];
+    load8<BF16>(src, row + e0, x);
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const f32x2 t = cs[(e0 >> 1) + j];
+      y[2 * j] = fmaf(x[2 * j], t[0], -x[2 * j + 1] * t[1]);
+      y[2 * j + 1] = fmaf(x[2 * j + 1], t[0], x[2 * j] * t[1]);
+    }
+    if (out) store8<BF16>(out, row + e0, y);
+    if (pool) store8<BF16>(pool, prow + e0, y);
+  }
+}
+
+template <bool BF16>
 __global__ void __launch_bounds__(256) rope_append_kernel(RopeArgs a) {
   __shared__ f32x2 cs[64];
   const int tok = blockIdx.x;
@@ -124,68 +186,25 @@ __global__ void __launch_bounds__(256) rope_append_kernel(RopeArgs a) {
   const int rot_units = rows * per_row;
   const int v_units = slot >= 0 ? a.Hkv * (d >> 3) : 0;
 
-  for (int u = threadIdx.x; u < rot_units + v_units; u += blockDim.x) {
-    if (u >= rot_units) {  // value row piece: bit copy into the cache
-      const int w = u - rot_units;
-      const int g = w / (d >> 3), e = (w - g * (d >> 3)) << 3;
-      copy8<BF16>(a.v_pool, a.v, (slot * a.Hkv + g) * d + e, ((int64_t)tok * a.Hkv + g) * d + e);
-      continue;
-    }
-    const int r = u / per_row, piece = u - r * per_row;
-    const bool is_q = r < nq;
-    const int h = is_q ? r : r - nq;
-    const void* src = is_q ? a.q : a.k;
-    const int64_t row = ((int64_t)tok * (is_q ? a.Hq : a.Hkv) + h) * d;
-    void* out = is_q ? a.q_out : a.k_out;
-    void* pool = is_q ? nullptr : (slot >= 0 ? a.k_pool : nullptr);
-    const int64_t prow = is_q ? 0 : (slot * a.Hkv + h) * d;
-    if (piece >= n_rot) {  // dims >= r: unchanged
-      const int e = a.rdim + ((piece - n_rot) << 3);
-      if (out) copy8<BF16>(out, src, row + e, row + e);
-      if (pool) copy8<BF16>(pool, src, prow + e, row + e);
-      continue;
-    }
-    if (neox) {
-      const int e0 = piece << 3, e1 = e0 + half;
-      float x0[8], x1[8], y0[8], y1[8];
-      load8<BF16>(src, row + e0, x0);
-      load8<BF16>(src, row + e1, x1);
-#pragma unroll
-      for (int j = 0; j < 8; ++j) {
-        const f32x2 t = cs[e0 + j];
-        y0[j] = fmaf(x0[j], t[0], -x1[j] * t[1]);
-        y1[j] = fmaf(x1[j], t[0], x0[j] * t[1]);
-      }
-      if (out) {
-        store8<BF16>(out, row + e0, y0);
-        store8<BF16>(out, row + e1, y1);
-      }
-      if (pool) {
-        store8<BF16>(pool, prow + e0, y0);
-        store8<BF16>(pool, prow + e1, y1);
-      }
-    } else {
-      const int e0 = piece << 3;
-      float x[8], y[8];
-      load8<BF16>(src, row + e0, x);
-#pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        const f32x2 t = cs[(e0 >> 1) + j];
-        y[2 * j] = fmaf(x[2 * j], t[0], -x[2 * j + 1] * t[1]);
-        y[2 * j + 1] = fmaf(x[2 * j + 1], t[0], x[2 * j] * t[1]);
-      }
-      if (out) store8<BF16>(out, row + e0, y);
-      if (pool) store8<BF16>(pool, prow + e0, y);
-    }
-  }
+  for (int u = blockIdx.y * blockDim.x + threadIdx.x; u < rot_units + v_units; u += gridDim.y * blockDim.x)
+    rotate_piece<BF16>(a, cs, tok, slot, u, rot_units, per_row, n_rot, nq, neox);
 }
 
 }  // namespace
 
 hipError_t launch_rope_append(const RopeArgs& a, int dtype_bf16, hipStream_t stream) {
   if (a.total_q == 0) return hipSuccess;
-  if (dtype_bf16) hipLaunchKernelGGL(rope_append_kernel<true>, dim3((unsigned)a.total_q), dim3(256), 0, stream, a);
-  else hipLaunchKernelGGL(rope_append_kernel<false>, dim3((unsigned)a.total_q), dim3(256), 0, stream, a);
+  // Upper bound of the pieces one token has (rows * pieces per row + value pieces).
+  const int pieces_per_row = (a.style == 1 ? a.rdim / 16 : a.rdim / 8) + (a.d - a.rdim) / 8;
+  const int units = ((a.q ? a.Hq : 0) + a.Hkv) * pieces_per_row + (a.k_pool ? a.Hkv * (a.d / 8) : 0);
+  // Slices per token: enough workgroups (~2048) to spread a short chunk over
+  // the chip, one when the chunk alone provides them.
+  const int max_slices = (units + 255) / 256;
+  int slices = (2048 + a.total_q - 1) / a.total_q;
+  if (slices > max_slices) slices = max_slices;
+  const dim3 grid((unsigned)a.total_q, (unsigned)slices);
+  if (dtype_bf16) hipLaunchKernelGGL(rope_append_kernel<true>, grid, dim3(256), 0, stream, a);
+  else hipLaunchKernelGGL(rope_append_kernel<false>, grid, dim3(256), 0, stream, a);
   return hipGetLastError();
 }
 
