@@ -30,6 +30,7 @@ from __future__ import annotations
 
 import argparse
 import ctypes
+import gc
 import hashlib
 import json
 import os
@@ -131,13 +132,152 @@ def cpu_baseline(case, target_s: float):
                        f"({fl / 1e9:.1f} GFLOP, {dt:.1f} s; full layer extrapolates to {full_s:.0f} s)")}
 
 
+def run_asr(args, torch, csr):
+    """Asynchronous state reconciliation (Algorithm 1) beside a stream of tasks.
+
+    One attention layer of the paper's setting: 100-token state chunks arrive
+    every ``--asr-period-ms``; each task extends the primary's cache by its
+    chunk plus a 16-token X_dyn (GQA 64q/4kv, d 128, bf16, RoPE theta 1e6);
+    at tau_mem = 110K cached tokens the oldest half of the chunks is evicted.
+    Task latency is completion minus scheduled arrival; the first ``skip``
+    tasks of every run (first-call allocations) are left out.  Runs from the
+    same state: no eviction; a blocking (stop-the-world) re-prefill on the
+    primary; ASR with the secondary confined to a CU partition and the primary
+    on the whole device (it finds the secondary's CUs busy while a
+    reconciliation runs); ASR with both on complementary partitions; ASR on two
+    unpartitioned streams.
+    """
+    from paper_2605_07325_amd import asr
+
+    HQ, HKV, D, P = 64, 4, 128, 16
+    PRE, CHUNK, DYN = 2048, 100, 16
+    lead = 40                                     # tasks before the eviction triggers
+    skip = 10                                     # warm-up tasks left out of the statistics
+    tau = args.asr_tau
+    start_chunks = (tau - PRE) // CHUNK - lead
+    max_tasks = 1500
+    n_tokens = PRE + (start_chunks + max_tasks) * CHUNK
+    dyn_base = n_tokens
+    log(f"asr: token table of {n_tokens + DYN * max_tasks} tokens (synthetic projections)")
+    table = asr.TokenTable.synthetic(n_tokens + DYN * max_tasks, HQ, HKV, D, seed=5)
+    desc = csr.make_desc(HQ, HKV, D, P, rope_style=csr.CSR_ROPE_NEOX, rope_theta=1e6)
+    sec_cus = asr.xcd_spread_cus(args.asr_secondary_cus_per_xcd)
+    prim_cus = sorted(set(range(256)) - set(sec_cus))
+    period = args.asr_period_ms * 1e-3
+
+    def run(mode):
+        if mode == "asr":
+            ps, ss = torch.cuda.Stream(), asr.cu_masked_stream(sec_cus)
+        elif mode == "asr_partitioned":
+            ps, ss = asr.cu_masked_stream(prim_cus), asr.cu_masked_stream(sec_cus)
+        else:
+            ps, ss = torch.cuda.Stream(), torch.cuda.Stream()
+        rec = asr.Reconciler(table, desc, (0, PRE), tau if mode != "steady" else 1 << 30, CHUNK,
+                             args.asr_cache_tokens, ps, ss, blocking=(mode == "blocking"))
+        chunks = [(PRE + CHUNK * i, PRE + CHUNK * (i + 1)) for i in range(start_chunks)]
+        rec.prime(chunks)
+        torch.cuda.synchronize()
+        gc.collect()
+        gc.disable()          # a serving loop: no collector pauses inside the timed region
+        rec.start_clock()
+        swap_at, i = None, 0
+        lag = []              # host submission minus scheduled arrival
+        while i < max_tasks:
+            t_arr = i * period
+            while rec.now() < t_arr:
+                pass
+            lag.append(rec.now() - t_arr)
+            c = start_chunks + i
+            rec.step((PRE + CHUNK * c, PRE + CHUNK * (c + 1)), (dyn_base + DYN * i, dyn_base + DYN * (i + 1)),
+                     arrival=t_arr)
+            if swap_at is None and any(e.kind == "swap" for e in rec.events):
+                swap_at = i
+            i += 1
+            if mode == "steady" and i >= lead + 200:
+                break
+            if swap_at is not None and i >= swap_at + args.asr_after_swap:
+                break
+        gc.enable()
+        full = np.asarray(rec.latencies_ms())
+        lat = full[skip:]
+        res = {"tasks": len(lat), "p50_ms": round(float(np.percentile(lat, 50)), 4),
+               "p99_ms": round(float(np.percentile(lat, 99)), 4), "max_ms": round(float(lat.max()), 4),
+               "mean_ms": round(float(lat.mean()), 4)}
+        # the same split by phase: before the eviction, while it is reconciled, after the swap
+        swap_task = next((e.task for e in rec.events if e.kind == "swap"), None)
+        phases = {"before": full[skip:lead + 1]}
+        if swap_task is not None:
+            phases["during"] = full[lead + 1:swap_task + 1]
+            phases["after"] = full[swap_task + 1:]
+        res["phases"] = {k: {"tasks": len(v), "p50_ms": round(float(np.percentile(v, 50)), 4),
+                             "max_ms": round(float(v.max()), 4)} for k, v in phases.items() if len(v)}
+        slow = [(int(j), round(float(x), 2)) for j, x in enumerate(full) if x > 5.0]
+        res["tasks_over_5ms"] = slow[:20]
+        lag_ms = np.asarray(lag) * 1e3
+        res["submit_lag_ms"] = {"p50": round(float(np.percentile(lag_ms, 50)), 4),
+                                "max": round(float(lag_ms.max()), 3), "argmax": int(lag_ms.argmax())}
+        if args.asr_dump:
+            np.save(os.path.join(args.asr_dump, f"asr_latency_{mode}.npy"), full)
+        if mode != "steady":
+            ev = [(e.kind, e.task, e.tokens) for e in rec.events]
+            res["events"] = [{"kind": k, "task": t, "tokens": n} for k, t, n in ev]
+            res["warmup_ms"] = [round(x, 2) for x in rec.warm_ms]
+            res["catchup_ms"] = [round(x, 2) for x in rec.catchup_ms]
+        log(f"asr {mode}: {res['tasks']} tasks, latency p50 {res['p50_ms']:.3f} ms, p99 {res['p99_ms']:.3f} ms, "
+            f"max {res['max_ms']:.3f} ms" + (f"; events {res.get('events')}" if mode != "steady" else ""))
+        del rec
+        torch.cuda.synchronize()
+        torch.cuda.empty_cache()
+        return res, lat
+
+    modes = {}
+    for mode in args.asr_modes.split(","):
+        modes[mode], lat = run(mode)
+    a = modes.get("asr") or next(iter(modes.values()))
+    x_dot = CHUNK / period                                    # tokens per second
+    n_buffer = args.asr_cache_tokens - tau
+    t_mem = n_buffer / x_dot
+    t_warm = sum(a.get("warmup_ms", [])) * 1e-3
+    t_recon = sum(a.get("catchup_ms", [])) * 1e-3
+    return {
+        "metric": "extend task latency p99 during state reconciliation (one layer, 100-token chunks at ~110K cache)",
+        "value": a["p99_ms"],
+        "unit": "ms",
+        "n_gpus": 1,
+        "steps": a["tasks"],
+        "warmup": 0,
+        "ms_per_step": a["mean_ms"],
+        "higher_is_better": False,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {
+            "workload": (f"asynchronous state reconciliation: tasks of a {CHUNK}-token state chunk + {DYN}-token "
+                         f"X_dyn every {args.asr_period_ms} ms, X_pre {PRE}, tau_mem {tau}, evict oldest half of "
+                         f"the chunks, N_catchup {CHUNK}, cache {args.asr_cache_tokens} tokens per resource; GQA "
+                         f"{HQ}q/{HKV}kv, head_dim {D}, page {P}, RoPE neox theta 1e6, one attention layer"),
+            "name": "asr",
+            "secondary_cus": len(sec_cus),
+            "primary_cus": len(prim_cus),
+        },
+        "modes": modes,
+        "theorem4": {
+            "x_dot_tokens_per_s": x_dot, "n_buffer_tokens": n_buffer,
+            "t_mem_s": round(t_mem, 4), "t_warm_s": round(t_warm, 4), "t_recon_s": round(t_recon, 4),
+            "viable": bool(t_warm + t_recon <= t_mem),
+        },
+    }
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=30)
     ap.add_argument("--warmup", type=int, default=10)
     ap.add_argument("--workload", default="c3_512",
-                    help="c3_<n> extend over a 122880 prefix (default n=512), c2, c5, c1, c4_<S> (prefill)")
+                    help="c3_<n> extend over a 122880 prefix (default n=512), c2, c5, c1, c4_<S> (prefill), "
+                         "asr (state reconciliation beside a stream of 100-token tasks)")
     ap.add_argument("--pools", type=int, default=3, help="K/V pool copies rotated across steps")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
@@ -146,6 +286,14 @@ def main():
                     help="rotate q and k_new at their absolute positions inside the step (fused with the append)")
     ap.add_argument("--rope-theta", type=float, default=1e6)
     ap.add_argument("--rope-dim", type=int, default=0, help="rotated dims (0 = head_dim)")
+    ap.add_argument("--asr-period-ms", type=float, default=2.0, help="asr: task arrival period")
+    ap.add_argument("--asr-secondary-cus-per-xcd", type=int, default=8, help="asr: secondary partition size")
+    ap.add_argument("--asr-tau", type=int, default=110000, help="asr: eviction threshold tau_mem (tokens)")
+    ap.add_argument("--asr-cache-tokens", type=int, default=163840, help="asr: cache capacity N_max per resource")
+    ap.add_argument("--asr-after-swap", type=int, default=100, help="asr: tasks served after the swap")
+    ap.add_argument("--asr-dump", default="", help="asr: directory for per-task latency arrays")
+    ap.add_argument("--asr-modes", default="steady,blocking,asr,asr_partitioned,asr_shared",
+                    help="asr: runs to make (the JSON value is the 'asr' run's p99)")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="also run a 1 GiB device copy (HBM counter calibration for rocprofv3 --pmc runs)")
     args = ap.parse_args()
@@ -165,6 +313,10 @@ def main():
     if not torch.cuda.is_available():
         print("bench.py needs an MI355X (no GPU visible)", file=sys.stderr)
         sys.exit(1)
+
+    if args.workload == "asr":
+        print(json.dumps(run_asr(args, torch, csr)), flush=True)
+        return
 
     t0 = time.perf_counter()
     case = dg.config(args.workload)

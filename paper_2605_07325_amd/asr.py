@@ -99,6 +99,13 @@ class TokenTable:
 
     def gather(self, ranges: List[Range]):
         """Rows for the ids in ``ranges`` (in order), as contiguous q, k, v."""
+        merged: List[Range] = []
+        for a, b in ranges:
+            if merged and merged[-1][1] == a:
+                merged[-1] = (merged[-1][0], b)
+            elif b > a:
+                merged.append((a, b))
+        ranges = merged
         if len(ranges) == 1:
             a, b = ranges[0]
             return self.q[a:b], self.k[a:b], self.v[a:b]
@@ -322,8 +329,17 @@ class Reconciler:
             self.events.append(Event("swap", task_index, rlen(self.pending), self.now()))
             return
 
+    def start_clock(self) -> None:
+        """Reference point for arrival times: an event on the primary stream,
+        waited for, and the host clock read right after it."""
+        self.ref_event = torch.cuda.Event(enable_timing=True)
+        self.ref_event.record(self.ps)
+        self.ref_event.synchronize()
+        self.t0 = time.perf_counter()
+
     def step(self, chunk: Range, dyn: Optional[Range] = None, arrival: Optional[float] = None) -> Task:
-        """One task: reconcile progress, Increment(chunk), inference on the primary."""
+        """One task: reconcile progress, Increment(chunk), inference on the primary.
+        ``arrival`` (seconds after ``start_clock``) defaults to now."""
         index = len(self.tasks)
         self._advance(index)
         self.chunks.append([chunk])
@@ -333,10 +349,7 @@ class Reconciler:
         cache = self.primary_cache()
         computed = self.pending + [chunk] + ([dyn] if dyn else [])
         if self.ref_event is None:
-            self.ref_event = torch.cuda.Event(enable_timing=True)
-            self.ref_event.record(self.ps)
-            self.ref_event.synchronize()
-            self.t0 = time.perf_counter()
+            self.start_clock()
         arrival = self.now() if arrival is None else arrival
         with torch.cuda.stream(self.ps):
             out, _ = self._extend(cache, computed, self.ps)
