@@ -36,6 +36,16 @@
  * through.  Keys already in the cache were rotated when they were appended, so
  * they are used as stored.
  *
+ * FP8 KV cache (optional): keys and values are stored as OCP e4m3 codes (1 sign,
+ * 4 exponent bits with bias 7, 3 mantissa bits; no infinities; S.1111.111 is
+ * NaN; largest finite 448) with one dequantisation scale per tensor:
+ * value = decode(code) * scale.  A value x (its bf16 or fp32 input value, or
+ * with RoPE its rotation rounded to fp32) is stored as
+ * code = nearest_even_e4m3(clamp(fp32(x * fp32(1 / scale)), -448, 448)).
+ * Chunk keys and values enter the attention through that same quantisation,
+ * so a key reads back identically whether it comes from the chunk or, on a
+ * later call, from the cache.
+ *
  * Paged cache layout (the library's contract; one convention for both sides):
  *   pool[num_pages][P][Hkv][d]; logical position t of sequence b lives in
  *   slot = page * P + (t mod P), page = block_table[b * bt_stride + t / P];
@@ -94,6 +104,45 @@ static uint16_t bf16_from_double(double v) {
   return (uint16_t)(bits >> 16);
 }
 
+/* OCP e4m3 code of an fp32 value: saturate to +-448, round to nearest even
+ * (subnormals in steps of 2^-9), NaN to 0x7f.  Evaluated exactly in double. */
+static uint8_t e4m3_encode(float x) {
+  if (isnan(x)) return 0x7f;
+  const uint8_t sign = signbit(x) ? 0x80 : 0x00;
+  double a = fabs((double)x);
+  if (a > 448.0) a = 448.0;
+  if (a < ldexp(1.0, -6)) return sign | (uint8_t)nearbyint(ldexp(a, 9)); /* 8 is the smallest normal */
+  int e;
+  (void)frexp(a, &e);              /* a in [2^(e-1), 2^e) */
+  int E = e - 1;
+  double m = nearbyint(ldexp(a, 3 - E)); /* significand in eighths: 8 .. 16 */
+  if (m == 16.0) { m = 8.0; E += 1; }
+  return sign | (uint8_t)(((E + 7) << 3) | ((int)m - 8));
+}
+
+static double e4m3_decode(uint8_t c) {
+  const int e = (c >> 3) & 15, m = c & 7;
+  if (e == 15 && m == 7) return NAN;
+  const double v = e == 0 ? ldexp((double)m, -9) : ldexp((double)(8 + m), e - 10);
+  return (c & 0x80) ? -v : v;
+}
+
+/* Stored code of an input value under dequantisation scale `scale`. */
+static uint8_t fp8_quantize(double x, float scale) {
+  const float inv = 1.0f / scale;
+  return e4m3_encode((float)x * inv);
+}
+
+int csr_oracle_e4m3_encode(const float* x, uint8_t* out, int64_t n) {
+  for (int64_t i = 0; i < n; ++i) out[i] = e4m3_encode(x[i]);
+  return 0;
+}
+
+int csr_oracle_e4m3_decode(const uint8_t* c, double* out, int64_t n) {
+  for (int64_t i = 0; i < n; ++i) out[i] = e4m3_decode(c[i]);
+  return 0;
+}
+
 /*
  * Rotate n_rows d-vectors, row k at position pos[k] (fp64 in, fp64 out).
  * Returns -1 for a malformed rotation (odd or out-of-range r, unknown pairing).
@@ -138,7 +187,8 @@ static int owner(const int32_t* cu, int batch, int tok) {
  * token outside every sequence, or -2 on allocation failure.
  */
 int csr_oracle_attention(int dtype, int Hq, int Hkv, int d, int P, double scale, int rope_style,
-                         int rope_dim, double rope_theta, int batch,
+                         int rope_dim, double rope_theta, int kv_fp8, float k_scale, float v_scale,
+                         int batch,
                          const void* q, const void* k_new, const void* v_new, const void* k_pool,
                          const void* v_pool, const int32_t* block_table, int bt_stride,
                          const int32_t* cu_seqlens_q, const int32_t* cache_len, int n_rows,
@@ -184,9 +234,15 @@ int csr_oracle_attention(int dtype, int Hq, int Hkv, int d, int P, double scale,
       const void* ksrc;
       if (t < L) { base = (cache_slot(block_table, bt_stride, P, b, t) * Hkv + g) * d; ksrc = k_pool; }
       else       { base = ((int64_t)(cu_seqlens_q[b] + (t - L)) * Hkv + g) * d; ksrc = k_new; }
-      for (int c = 0; c < d; ++c) raw[c] = widen(ksrc, base + c, dtype);
-      if (t < L) memcpy(kv, raw, sizeof(double) * (size_t)d);
-      else rope_row(raw, kv, d, rope_dim, rope_style, rope_theta, t);
+      if (t < L && kv_fp8) {
+        for (int c = 0; c < d; ++c) kv[c] = e4m3_decode(((const uint8_t*)ksrc)[base + c]) * (double)k_scale;
+      } else {
+        for (int c = 0; c < d; ++c) raw[c] = widen(ksrc, base + c, dtype);
+        if (t < L) memcpy(kv, raw, sizeof(double) * (size_t)d);
+        else rope_row(raw, kv, d, rope_dim, rope_style, rope_theta, t);
+        if (t >= L && kv_fp8) /* a chunk key enters as it will be cached */
+          for (int c = 0; c < d; ++c) kv[c] = e4m3_decode(fp8_quantize(kv[c], k_scale)) * (double)k_scale;
+      }
       for (int j = 0; j < G; ++j) {
         double dot = 0.0;
         for (int c = 0; c < d; ++c) dot += qv[j * d + c] * kv[c];
@@ -209,7 +265,13 @@ int csr_oracle_attention(int dtype, int Hq, int Hkv, int d, int P, double scale,
       const void* vsrc;
       if (t < L) { base = (cache_slot(block_table, bt_stride, P, b, t) * Hkv + g) * d; vsrc = v_pool; }
       else       { base = ((int64_t)(cu_seqlens_q[b] + (t - L)) * Hkv + g) * d; vsrc = v_new; }
-      for (int c = 0; c < d; ++c) kv[c] = widen(vsrc, base + c, dtype);
+      if (t < L && kv_fp8)
+        for (int c = 0; c < d; ++c) kv[c] = e4m3_decode(((const uint8_t*)vsrc)[base + c]) * (double)v_scale;
+      else if (kv_fp8)
+        for (int c = 0; c < d; ++c)
+          kv[c] = e4m3_decode(fp8_quantize(widen(vsrc, base + c, dtype), v_scale)) * (double)v_scale;
+      else
+        for (int c = 0; c < d; ++c) kv[c] = widen(vsrc, base + c, dtype);
       for (int j = 0; j < G; ++j) {
         const double w = s[j * nkeys + t];
         for (int c = 0; c < d; ++c) acc[j * d + c] += w * kv[c];
@@ -232,12 +294,15 @@ int csr_oracle_attention(int dtype, int Hq, int Hkv, int d, int P, double scale,
  * other byte of either pool changes.  Values are copied bit for bit; keys too
  * unless rope_style != ROPE_NONE, in which case each key row is first rotated
  * at its position L_b + i (in double precision) and rounded to the pool's
- * element type (nearest, ties to even).
+ * element type (nearest, ties to even).  With kv_fp8 the pools hold e4m3
+ * codes: keys (rotated and rounded to fp32 first when RoPE is on) and values
+ * are quantised as the file comment defines.
  */
 int csr_oracle_kv_append(int dtype, int Hkv, int d, int P, int rope_style, int rope_dim,
-                         double rope_theta, int batch, const void* k_new, const void* v_new,
-                         void* k_pool, void* v_pool, const int32_t* block_table, int bt_stride,
-                         const int32_t* cu_seqlens_q, const int32_t* cache_len) {
+                         double rope_theta, int kv_fp8, float k_scale, float v_scale, int batch,
+                         const void* k_new, const void* v_new, void* k_pool, void* v_pool,
+                         const int32_t* block_table, int bt_stride, const int32_t* cu_seqlens_q,
+                         const int32_t* cache_len) {
   const int elem_bytes = dtype == ORACLE_BF16 ? 2 : 4;
   const size_t row = (size_t)Hkv * d * elem_bytes; /* one token: all kv heads */
   double* raw = (double*)malloc(sizeof(double) * (size_t)d);
@@ -248,6 +313,18 @@ int csr_oracle_kv_append(int dtype, int Hkv, int d, int P, int rope_style, int r
     for (int64_t i = 0; i < cu_seqlens_q[b + 1] - cu_seqlens_q[b]; ++i) {
       const int64_t slot = cache_slot(block_table, bt_stride, P, b, L + i);
       const int64_t src = cu_seqlens_q[b] + i;
+      if (kv_fp8) {
+        for (int g = 0; g < Hkv; ++g) {
+          for (int c = 0; c < d; ++c) raw[c] = widen(k_new, (src * Hkv + g) * d + c, dtype);
+          rope_row(raw, rot, d, rope_dim, rope_style, rope_theta, L + i);
+          for (int c = 0; c < d; ++c) {
+            const int64_t e = (slot * Hkv + g) * d + c;
+            ((uint8_t*)k_pool)[e] = fp8_quantize(rot[c], k_scale);
+            ((uint8_t*)v_pool)[e] = fp8_quantize(widen(v_new, (src * Hkv + g) * d + c, dtype), v_scale);
+          }
+        }
+        continue;
+      }
       memcpy((char*)v_pool + slot * row, (const char*)v_new + src * row, row);
       if (rope_style == ROPE_NONE) {
         memcpy((char*)k_pool + slot * row, (const char*)k_new + src * row, row);

@@ -36,10 +36,15 @@ def _load():
             build()
         lib = ctypes.CDLL(LIB)
         p, i, d = ctypes.c_void_p, ctypes.c_int, ctypes.c_double
-        lib.csr_oracle_attention.argtypes = [i, i, i, i, i, d, i, i, d, i, p, p, p, p, p, p, i, p, p, i, p, p, p,
-                                             p, i]
+        f = ctypes.c_float
+        lib.csr_oracle_attention.argtypes = [i, i, i, i, i, d, i, i, d, i, f, f, i, p, p, p, p, p, p, i, p, p, i, p,
+                                             p, p, p, i]
         lib.csr_oracle_attention.restype = i
-        lib.csr_oracle_kv_append.argtypes = [i, i, i, i, i, i, d, i, p, p, p, p, p, i, p, p]
+        lib.csr_oracle_kv_append.argtypes = [i, i, i, i, i, i, d, i, f, f, i, p, p, p, p, p, i, p, p]
+        lib.csr_oracle_e4m3_encode.argtypes = [p, p, ctypes.c_int64]
+        lib.csr_oracle_e4m3_encode.restype = i
+        lib.csr_oracle_e4m3_decode.argtypes = [p, p, ctypes.c_int64]
+        lib.csr_oracle_e4m3_decode.restype = i
         lib.csr_oracle_kv_append.restype = i
         lib.csr_oracle_rope.argtypes = [p, p, ctypes.c_int64, i, i, i, d, p]
         lib.csr_oracle_rope.restype = i
@@ -67,6 +72,30 @@ def _rope_args(rope, head_dim):
     return int(style), int(r or head_dim), float(base)
 
 
+def _fp8_args(fp8):
+    """``fp8`` = None (pools in the input type) or ``(k_scale, v_scale)``:
+    pools of OCP e4m3 codes (uint8) with those dequantisation scales."""
+    if fp8 is None:
+        return 0, 1.0, 1.0
+    return 1, float(fp8[0]), float(fp8[1])
+
+
+def e4m3_encode(x):
+    """OCP e4m3 codes of fp32 values: saturate to +-448, nearest even."""
+    x = np.ascontiguousarray(x, dtype=np.float32)
+    out = np.empty(x.shape, np.uint8)
+    _load().csr_oracle_e4m3_encode(_ptr(x), _ptr(out), x.size)
+    return out
+
+
+def e4m3_decode(codes):
+    """Exact values (float64) of OCP e4m3 codes."""
+    c = np.ascontiguousarray(codes, dtype=np.uint8)
+    out = np.empty(c.shape, np.float64)
+    _load().csr_oracle_e4m3_decode(_ptr(c), _ptr(out), c.size)
+    return out
+
+
 def rope(x, positions, style, rotary_dims, base):
     """RoFormer's rotary position embedding (Su et al., 2021) of fp64 rows
     ``x [R, d]`` (or ``[R, H, d]``, one position per leading row) at
@@ -89,7 +118,7 @@ def rope(x, positions, style, rotary_dims, base):
 
 def attention(dtype, q, k_new, v_new, k_pool, v_pool, block_table, bt_stride, cu_seqlens_q,
               cache_len, rows, num_q_heads, num_kv_heads, head_dim, page_size, scale=None,
-              nthreads=None, rope=None):
+              nthreads=None, rope=None, fp8=None):
     """Extend attention for the query tokens in ``rows`` (all heads).
 
     Paper Sec. II, eq. (causal_attention_1)-(causal_attention_3) over the
@@ -98,8 +127,10 @@ def attention(dtype, q, k_new, v_new, k_pool, v_pool, block_table, bt_stride, cu
     (warm-up of Algorithm 1).  Arrays: bf16 as uint16 bit patterns, fp32 as
     float32.  ``rope=(style, rotary_dims, base)`` first rotates every query
     row and every chunk key at its absolute position (see ``rope``); cached
-    keys are used as stored.  Returns ``(out [R,Hq,d] f64, lse [R,Hq] f64,
-    pairs [R,Hq] i64)``.
+    keys are used as stored.  ``fp8=(k_scale, v_scale)``: the pools hold e4m3
+    codes (uint8) and chunk keys/values enter quantised exactly as the append
+    stores them.  Returns ``(out [R,Hq,d] f64, lse [R,Hq] f64, pairs [R,Hq]
+    i64)``.
     """
     lib = _load()
     G = num_q_heads // num_kv_heads
@@ -116,7 +147,7 @@ def attention(dtype, q, k_new, v_new, k_pool, v_pool, block_table, bt_stride, cu
     cl = _i32(cache_len)
     rc = lib.csr_oracle_attention(
         dtype, num_q_heads, num_kv_heads, head_dim, page_size, 0.0 if scale is None else float(scale),
-        *_rope_args(rope, head_dim), int(cu.shape[0] - 1), *[_ptr(a) for a in arrs], _ptr(bt), int(bt_stride), _ptr(cu), _ptr(cl),
+        *_rope_args(rope, head_dim), *_fp8_args(fp8), int(cu.shape[0] - 1), *[_ptr(a) for a in arrs], _ptr(bt), int(bt_stride), _ptr(cu), _ptr(cl),
         R, _ptr(rows), _ptr(out), _ptr(lse), _ptr(pairs), int(nthreads or default_threads()))
     if rc != 0:
         raise RuntimeError(f"oracle attention failed ({rc})")
@@ -124,11 +155,13 @@ def attention(dtype, q, k_new, v_new, k_pool, v_pool, block_table, bt_stride, cu
 
 
 def kv_append(k_new, v_new, k_pool, v_pool, block_table, bt_stride, cu_seqlens_q, cache_len,
-              num_kv_heads, head_dim, page_size, rope=None):
+              num_kv_heads, head_dim, page_size, rope=None, fp8=None):
     """Append oracle, in place on copies: Theorem 2's T (+) dX as a bit copy of
     each chunk row into cache position L_b + i.  With ``rope`` the key rows are
     rotated at that position and rounded to the pool's type (nearest, ties to
-    even) instead.  bf16 as uint16 bit patterns.  Returns the new pools."""
+    even) instead.  ``fp8=(k_scale, v_scale)``: the pools hold e4m3 codes and
+    both keys and values are quantised.  bf16 as uint16 bit patterns.  Returns
+    the new pools."""
     lib = _load()
     kp = np.array(k_pool, copy=True)
     vp = np.array(v_pool, copy=True)
@@ -139,7 +172,7 @@ def kv_append(k_new, v_new, k_pool, v_pool, block_table, bt_stride, cu_seqlens_q
     cl = _i32(cache_len)
     dt = {np.dtype(np.uint16): BF16, np.dtype(np.float32): F32}[kn.dtype]
     rc = lib.csr_oracle_kv_append(dt, num_kv_heads, head_dim, page_size, *_rope_args(rope, head_dim),
-                                  int(cu.shape[0] - 1),
+                                  *_fp8_args(fp8), int(cu.shape[0] - 1),
                                   _ptr(kn), _ptr(vn), _ptr(kp), _ptr(vp), _ptr(bt), int(bt_stride),
                                   _ptr(cu), _ptr(cl))
     if rc != 0:

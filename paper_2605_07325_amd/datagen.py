@@ -28,6 +28,42 @@ CANARY_BF16 = np.uint16(0xFFFF)
 CANARY_F32 = np.uint32(0xFFFFFFFF)
 
 
+# e4m3 NaN (S.1111.111): marks slots of an fp8 pool that hold no token yet.
+CANARY_FP8 = np.uint8(0xFF)
+
+
+def fp8_codes(g: np.random.Generator, shape, exp_lo: int = 3, exp_hi: int = 9) -> np.ndarray:
+    """Random OCP e4m3 bit patterns (uint8): random sign and mantissa, biased
+    exponent field uniform in [exp_lo, exp_hi], so magnitudes lie in
+    [2^(exp_lo-7), 2^(exp_hi-6)) before the pool's scale; never NaN."""
+    sign = g.integers(0, 2, size=shape, dtype=np.uint8) << 7
+    expo = g.integers(exp_lo, exp_hi + 1, size=shape, dtype=np.uint8) << 3
+    mant = g.integers(0, 8, size=shape, dtype=np.uint8)
+    return (sign | expo | mant).astype(np.uint8)
+
+
+def with_fp8_pools(case: "Case", cfg_id: int = 0) -> "Case":
+    """The same workload with e4m3 pools: every slot that holds a prefix
+    token gets random codes (``fp8_codes``), every other slot the NaN canary.
+    The chunk's K/V stay in the case's input type."""
+    import dataclasses
+    P = case.page_size
+    shape = case.k_pool.shape
+    k8 = np.full(shape, CANARY_FP8, np.uint8)
+    v8 = np.full(shape, CANARY_FP8, np.uint8)
+    for b in range(case.batch):
+        L = int(case.cache_len[b])
+        if L == 0:
+            continue
+        t = np.arange(L, dtype=np.int64)
+        page = (case.block_table[b, t // P].astype(np.int64) if case.block_table is not None
+                else b * case.bt_stride + t // P)
+        slots = page * P + t % P
+        k8.reshape(-1, shape[2], shape[3])[slots] = fp8_codes(rng(case.seed, cfg_id, 300 + 2 * b), (L, shape[2], shape[3]))
+        v8.reshape(-1, shape[2], shape[3])[slots] = fp8_codes(rng(case.seed, cfg_id, 301 + 2 * b), (L, shape[2], shape[3]))
+    return dataclasses.replace(case, k_pool=k8, v_pool=v8, k_prefix=None, v_prefix=None)
+
+
 def rng(seed: int, cfg_id: int, tensor_id: int) -> np.random.Generator:
     return np.random.Generator(np.random.PCG64(np.random.SeedSequence([seed, cfg_id, tensor_id])))
 
