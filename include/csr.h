@@ -30,12 +30,24 @@
  * in fp64) and rounded to the element type (nearest, ties to even).  Keys that
  * are already in the cache are read as stored.
  *
+ * FP8 KV cache (optional, csr_attn_desc.kv_dtype = CSR_KV_FP8_E4M3): the pools
+ * hold OCP e4m3 codes (1 byte: sign, 4 exponent bits with bias 7, 3 mantissa
+ * bits, no infinities, S.1111.111 = NaN, largest finite 448), one byte per
+ * element, with one dequantisation scale per tensor: a cached key is
+ * code * k_scale, a value code * v_scale.  The chunk's keys (after RoPE) and
+ * values arrive in bf16 and are stored as
+ * e4m3_nearest_even(clamp(x * fp32(1 / scale), -448, 448)); the attention
+ * reads the chunk through that same quantisation, so a key is identical
+ * whether it comes from the chunk or, on a later call, from the cache.  The
+ * attention converts codes to bf16 exactly and computes as for bf16 (fp32
+ * accumulation); q and the output stay bf16.  Needs dtype CSR_BF16, d = 128.
+ *
  * Memory layout (all row-major, element type per csr_attn_desc.dtype):
  *   q                 [T_q][Hq][d]        T_q = cu_seqlens_q[batch]
  *   k_new, v_new      [T_q][Hkv][d]
  *   out               [T_q][Hq][d]        same element type as q
  *   lse               [T_q][Hq]           float (natural log), optional
- *   k_pool, v_pool    [num_pages][P][Hkv][d]
+ *   k_pool, v_pool    [num_pages][P][Hkv][d]   (uint8 codes with an fp8 cache)
  *   block_table       [batch][bt_stride]  int32 page ids
  * Position t of sequence b lives in pool slot page * P + t % P with
  * page = block_table[b * bt_stride + t / P].  A NULL block_table means the
@@ -81,6 +93,12 @@ typedef enum { CSR_F32 = 0, CSR_BF16 = 1 } csr_dtype;
 /* csr_extend_attention flags */
 #define CSR_APPEND 1u /* also append the chunk's K/V to the cache (csr_kv_append) */
 
+/* csr_attn_desc.kv_dtype */
+typedef enum {
+  CSR_KV_SAME = 0,      /* the cache holds the input type (csr_attn_desc.dtype) */
+  CSR_KV_FP8_E4M3 = 1   /* OCP e4m3 codes with per-tensor scales k_scale, v_scale */
+} csr_kv_dtype;
+
 /* csr_attn_desc.rope_style */
 typedef enum {
   CSR_ROPE_NONE = 0,        /* q and k arrive already carrying their positions */
@@ -99,6 +117,9 @@ typedef struct {
   int32_t rope_style;    /* csr_rope_style; 0 (all fields zero) = no rotation */
   int32_t rope_dim;      /* r: rotated leading dims, a multiple of 16 in [16, d]; 0 = d */
   float rope_theta;      /* base of the pair frequencies, finite and > 0 (e.g. 1e4, 1e6) */
+  int32_t kv_dtype;      /* csr_kv_dtype; 0 = the cache holds the input type */
+  float k_scale;         /* fp8 cache: key dequantisation scale, finite and > 0 */
+  float v_scale;         /* fp8 cache: value dequantisation scale, finite and > 0 */
 } csr_attn_desc;
 
 /*
@@ -110,7 +131,8 @@ typedef struct {
  * so every cached position < L_b stays as it was.  With desc->rope_style set,
  * each key row is rotated at its position L_b + i and rounded to the element
  * type instead of copied (values are still copied bit for bit); the pass is
- * fused into the same launch.  Committing the appended
+ * fused into the same launch.  With an fp8 cache (desc->kv_dtype) keys and
+ * values are quantised as the file comment defines.  Committing the appended
  * rows (advancing L_b) is the caller's choice: rows of the dynamic suffix are
  * simply overwritten by the next call.
  *   cu_seqlens_q   [batch+1] device int32 prefix sums of n_b
@@ -127,9 +149,10 @@ csr_status csr_kv_append(const csr_attn_desc* desc, int32_t batch, const void* k
 
 /*
  * Workspace bytes csr_extend_attention needs for these sizes: split-K
- * partials when the plan splits the key range, plus rotated copies of q and
- * k_new ([T_q][Hq][d] and [T_q][Hkv][d], 256-byte aligned) when
- * desc->rope_style is set; 0 when neither applies.  The same host integers
+ * partials when the plan splits the key range, plus the prepared chunk when
+ * RoPE or an fp8 cache is set (each part 256-byte aligned): rotated q
+ * [T_q][Hq][d] (RoPE), prepared k [T_q][Hkv][d] (rotated and/or e4m3), e4m3
+ * v [T_q][Hkv][d] (fp8 cache); 0 when none applies.  The same host integers
  * must be passed to the call.
  */
 size_t csr_extend_workspace_size(const csr_attn_desc* desc, int32_t batch, int32_t total_q,
@@ -149,7 +172,8 @@ size_t csr_extend_workspace_size(const csr_attn_desc* desc, int32_t batch, int32
  *   q, k_new          with desc->rope_style set: unrotated projections; one
  *                     fused launch writes their rotations at L_b + i to the
  *                     workspace (and, with CSR_APPEND, the rotated keys and
- *                     the values to the cache) before the attention
+ *                     the values to the cache) before the attention; with an
+ *                     fp8 cache the same launch quantises k_new and v_new
  *   out               [T_q][Hq][d], element type of q
  *   lse               [T_q][Hq] float or NULL
  *   workspace         device scratch of >= csr_extend_workspace_size() bytes

@@ -20,6 +20,7 @@ CSR_OK, CSR_E_INVAL, CSR_E_UNSUPPORTED, CSR_E_WORKSPACE, CSR_E_HIP = 0, 1, 2, 3,
 CSR_F32, CSR_BF16 = 0, 1
 CSR_APPEND = 1
 CSR_ROPE_NONE, CSR_ROPE_NEOX, CSR_ROPE_INTERLEAVED = 0, 1, 2
+CSR_KV_SAME, CSR_KV_FP8_E4M3 = 0, 1
 
 # Every function include/csr.h declares.
 EXPORTS = ("csr_kv_append", "csr_extend_workspace_size", "csr_extend_attention", "csr_prefill_workspace_size",
@@ -29,7 +30,8 @@ EXPORTS = ("csr_kv_append", "csr_extend_workspace_size", "csr_extend_attention",
 class AttnDesc(ctypes.Structure):
     _fields_ = [("num_q_heads", ctypes.c_int32), ("num_kv_heads", ctypes.c_int32), ("head_dim", ctypes.c_int32),
                 ("page_size", ctypes.c_int32), ("softmax_scale", ctypes.c_float), ("dtype", ctypes.c_int32),
-                ("rope_style", ctypes.c_int32), ("rope_dim", ctypes.c_int32), ("rope_theta", ctypes.c_float)]
+                ("rope_style", ctypes.c_int32), ("rope_dim", ctypes.c_int32), ("rope_theta", ctypes.c_float),
+                ("kv_dtype", ctypes.c_int32), ("k_scale", ctypes.c_float), ("v_scale", ctypes.c_float)]
 
 
 class CsrError(RuntimeError):
@@ -89,13 +91,15 @@ def set_attention_events(begin_event, end_event) -> None:
 
 def make_desc(num_q_heads: int, num_kv_heads: int, head_dim: int, page_size: int = 16, dtype=torch.bfloat16,
               softmax_scale: float = 0.0, rope_style: int = CSR_ROPE_NONE, rope_dim: int = 0,
-              rope_theta: float = 0.0) -> AttnDesc:
+              rope_theta: float = 0.0, kv_dtype: int = CSR_KV_SAME, k_scale: float = 0.0,
+              v_scale: float = 0.0) -> AttnDesc:
     """csr_attn_desc.  ``rope_style`` != CSR_ROPE_NONE makes the library rotate q
     and k_new at their absolute positions (``rope_dim`` dims, 0 = all; base
-    ``rope_theta``)."""
+    ``rope_theta``); ``kv_dtype`` = CSR_KV_FP8_E4M3 keeps the cache as e4m3
+    codes (uint8 pools) with dequantisation scales ``k_scale``, ``v_scale``."""
     dt = {torch.bfloat16: CSR_BF16, torch.float32: CSR_F32}.get(dtype, dtype)
     return AttnDesc(num_q_heads, num_kv_heads, head_dim, page_size, softmax_scale, int(dt), int(rope_style),
-                    int(rope_dim), float(rope_theta))
+                    int(rope_dim), float(rope_theta), int(kv_dtype), float(k_scale), float(v_scale))
 
 
 def _ptr(t: Optional[torch.Tensor]):

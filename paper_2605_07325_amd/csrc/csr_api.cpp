@@ -63,34 +63,59 @@ csr_status check_desc(const csr_attn_desc* d) {
     if (!(d->rope_theta > 0.f) || isinf(d->rope_theta))
       return fail(CSR_E_INVAL, "rope_theta must be finite and > 0");
   }
+  if (d->kv_dtype != CSR_KV_SAME) {
+    if (d->kv_dtype != CSR_KV_FP8_E4M3) return fail(CSR_E_INVAL, "unknown kv_dtype %d", d->kv_dtype);
+    if (d->dtype != CSR_BF16 || d->head_dim != 128)
+      return fail(CSR_E_UNSUPPORTED, "an fp8 cache needs bf16 inputs and head_dim 128");
+    if (!(d->k_scale > 0.f) || isinf(d->k_scale) || !(d->v_scale > 0.f) || isinf(d->v_scale))
+      return fail(CSR_E_INVAL, "k_scale and v_scale must be finite and > 0");
+  }
   return CSR_OK;
 }
 
 bool has_rope(const csr_attn_desc* d) { return d->rope_style != CSR_ROPE_NONE; }
+bool kv_fp8(const csr_attn_desc* d) { return d->kv_dtype == CSR_KV_FP8_E4M3; }
+// RoPE or an fp8 cache: one launch prepares q/k/v (and appends) before the attention.
+bool needs_prep(const csr_attn_desc* d) { return has_rope(d) || kv_fp8(d); }
 
 size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 
 int elem_bytes(const csr_attn_desc* d) { return d->dtype == CSR_BF16 ? 2 : 4; }
 
-// Workspace head used by RoPE: rotated q, then rotated k (each 256-aligned).
-size_t rope_q_bytes(const csr_attn_desc* d, int total) {
-  return align256((size_t)total * d->num_q_heads * d->head_dim * elem_bytes(d));
-}
-size_t rope_ws_bytes(const csr_attn_desc* d, int total) {
-  if (!has_rope(d)) return 0;
-  return rope_q_bytes(d, total) + align256((size_t)total * d->num_kv_heads * d->head_dim * elem_bytes(d));
+// Workspace head written by the prep launch, each part 256-aligned: rotated q
+// (RoPE only), prepared k (rotated and/or quantised), quantised v (fp8 only).
+struct PrepLayout {
+  size_t q_off, k_off, v_off, bytes;
+};
+PrepLayout prep_layout(const csr_attn_desc* d, int total) {
+  PrepLayout l{0, 0, 0, 0};
+  if (!needs_prep(d)) return l;
+  const size_t rows = (size_t)total * d->head_dim;
+  const size_t qb = has_rope(d) ? align256(rows * d->num_q_heads * elem_bytes(d)) : 0;
+  const size_t kb = align256(rows * d->num_kv_heads * (kv_fp8(d) ? 1 : elem_bytes(d)));
+  const size_t vb = kv_fp8(d) ? align256(rows * d->num_kv_heads) : 0;
+  l.q_off = 0;
+  l.k_off = qb;
+  l.v_off = qb + kb;
+  l.bytes = qb + kb + vb;
+  return l;
 }
 
-// q / q_out may be NULL (keys only), k_pool NULL (no cache write).
+// q / q_out may be NULL (keys only), k_out / v_out NULL (no workspace copy),
+// k_pool NULL (no cache write).
 csr::RopeArgs rope_args(const csr_attn_desc* d, int batch, const void* q, const void* k, const void* v, void* q_out,
-                        void* k_out, void* k_pool, void* v_pool, int num_pages, const int32_t* bt, int bt_stride,
-                        const int32_t* cu, const int32_t* cache_len, int total) {
+                        void* k_out, void* v_out, void* k_pool, void* v_pool, int num_pages, const int32_t* bt,
+                        int bt_stride, const int32_t* cu, const int32_t* cache_len, int total) {
   csr::RopeArgs a;
-  a.q = q;
+  a.q = has_rope(d) ? q : nullptr;
   a.k = k;
   a.v = v;
-  a.q_out = q_out;
+  a.q_out = has_rope(d) ? q_out : nullptr;
   a.k_out = k_out;
+  a.v_out = kv_fp8(d) ? v_out : nullptr;
+  a.kv8 = kv_fp8(d) ? 1 : 0;
+  a.inv_k = kv_fp8(d) ? 1.f / d->k_scale : 1.f;
+  a.inv_v = kv_fp8(d) ? 1.f / d->v_scale : 1.f;
   a.k_pool = k_pool;
   a.v_pool = v_pool;
   a.block_table = bt;
@@ -104,7 +129,7 @@ csr::RopeArgs rope_args(const csr_attn_desc* d, int batch, const void* q, const 
   a.Hkv = d->num_kv_heads;
   a.d = d->head_dim;
   a.log2P = ilog2(d->page_size);
-  a.rdim = d->rope_dim ? d->rope_dim : d->head_dim;
+  a.rdim = has_rope(d) ? (d->rope_dim ? d->rope_dim : d->head_dim) : 0;
   a.style = d->rope_style;
   // Pair i turns by pos * theta^(-2i/r) radians: store that rate in half-turns.
   for (int i = 0; i < 64; ++i)
@@ -263,7 +288,11 @@ csr_status run_attention(const csr_attn_desc* d, int batch, const void* q, const
   a.d = d->head_dim;
   a.P = d->page_size;
   a.log2P = ilog2(d->page_size);
-  a.scale_log2 = scale * 1.4426950408889634f;
+  // an fp8 cache holds K / k_scale and V / v_scale: the scales come back in the
+  // score scale and in the output
+  a.scale_log2 = scale * 1.4426950408889634f * (kv_fp8(d) ? d->k_scale : 1.f);
+  a.v_scale = kv_fp8(d) ? d->v_scale : 1.f;
+  a.kv_fp8 = kv_fp8(d) ? 1 : 0;
   a.batch = batch;
   a.total_q = total_q;
   a.mtiles = p.mtiles;
@@ -328,11 +357,11 @@ csr_status csr_kv_append(const csr_attn_desc* desc, int32_t batch, const void* k
   st = check_pool(desc, k_pool, v_pool, num_pages, block_table, bt_stride, 0, "kv_append");
   if (st != CSR_OK) return st;
   if (cache_seqlens && !aligned4(cache_seqlens)) return fail(CSR_E_INVAL, "cache_seqlens must be 4-byte aligned");
-  if (has_rope(desc)) {
-    const csr::RopeArgs r = rope_args(desc, batch, nullptr, k_new, v_new, nullptr, nullptr, k_pool, v_pool,
+  if (needs_prep(desc)) {
+    const csr::RopeArgs r = rope_args(desc, batch, nullptr, k_new, v_new, nullptr, nullptr, nullptr, k_pool, v_pool,
                                       num_pages, block_table, bt_stride, cu_seqlens_q, cache_seqlens, total_q);
     return launched(csr::launch_rope_append(r, desc->dtype == CSR_BF16, static_cast<hipStream_t>(stream)),
-                    "rope kv_append");
+                    "prepared kv_append");
   }
   const csr::AppendArgs a = append_args(desc, batch, k_new, v_new, k_pool, v_pool, num_pages, block_table, bt_stride,
                                         cu_seqlens_q, cache_seqlens, total_q);
@@ -344,7 +373,7 @@ size_t csr_extend_workspace_size(const csr_attn_desc* desc, int32_t batch, int32
   if (check_desc(desc) != CSR_OK || batch < 1 || total_q < 1 || max_seqlen_q < 1 || max_cache_len < 0) return 0;
   Plan p;
   if (make_plan(desc, batch, total_q, max_seqlen_q, max_cache_len, p) != CSR_OK) return 0;
-  return rope_ws_bytes(desc, total_q) + p.ws_bytes;
+  return prep_layout(desc, total_q).bytes + p.ws_bytes;
 }
 
 size_t csr_prefill_workspace_size(const csr_attn_desc* desc, int32_t batch, int32_t total, int32_t max_seqlen) {
@@ -380,29 +409,29 @@ csr_status csr_extend_attention(const csr_attn_desc* desc, int32_t batch, const 
   Plan p;
   st = make_plan(desc, batch, total_q, max_seqlen_q, max_cache_len, p);
   if (st != CSR_OK) return st;
-  const size_t rope_bytes = rope_ws_bytes(desc, total_q);
-  if (rope_bytes + p.ws_bytes > 0) {
-    if (!workspace || workspace_bytes < rope_bytes + p.ws_bytes)
-      return fail(CSR_E_WORKSPACE, "workspace of %zu bytes required, got %zu", rope_bytes + p.ws_bytes,
+  const PrepLayout pl = prep_layout(desc, total_q);
+  if (pl.bytes + p.ws_bytes > 0) {
+    if (!workspace || workspace_bytes < pl.bytes + p.ws_bytes)
+      return fail(CSR_E_WORKSPACE, "workspace of %zu bytes required, got %zu", pl.bytes + p.ws_bytes,
                   workspace ? workspace_bytes : (size_t)0);
     if (!aligned16(workspace)) return fail(CSR_E_INVAL, "workspace must be 16-byte aligned");
   }
   const bool append = (flags & CSR_APPEND) != 0;
-  if (rope_bytes > 0) {
-    // Rotate q and k_new at L_b + i into the workspace (and append) in one launch,
-    // then attend over the rotated copies.
+  if (pl.bytes > 0) {
+    // One launch rotates q and k_new at L_b + i and/or quantises k_new and
+    // v_new into the workspace (and appends); the attention then reads the
+    // prepared copies.
     char* ws = static_cast<char*>(workspace);
-    void* q_rot = ws;
-    void* k_rot = ws + rope_q_bytes(desc, total_q);
-    const csr::RopeArgs r = rope_args(desc, batch, q, k_new, v_new, q_rot, k_rot, append ? k_pool : nullptr,
-                                      append ? v_pool : nullptr, num_pages, block_table, bt_stride, cu_seqlens_q,
-                                      cache_seqlens, total_q);
-    st = launched(csr::launch_rope_append(r, desc->dtype == CSR_BF16, s), "rope");
+    const bool rope = has_rope(desc), fp8 = kv_fp8(desc);
+    const csr::RopeArgs r = rope_args(desc, batch, q, k_new, v_new, ws + pl.q_off, ws + pl.k_off, ws + pl.v_off,
+                                      append ? k_pool : nullptr, append ? v_pool : nullptr, num_pages, block_table,
+                                      bt_stride, cu_seqlens_q, cache_seqlens, total_q);
+    st = launched(csr::launch_rope_append(r, desc->dtype == CSR_BF16, s), "prep");
     if (st != CSR_OK) return st;
-    return run_attention(desc, batch, q_rot, k_rot, v_new, k_pool, v_pool, num_pages, block_table, bt_stride,
-                         cu_seqlens_q, max_cache_len > 0 ? cache_seqlens : nullptr, total_q, max_seqlen_q,
-                         max_cache_len, out, lse, p.ws_bytes ? ws + rope_bytes : nullptr, workspace_bytes - rope_bytes,
-                         s);
+    return run_attention(desc, batch, rope ? ws + pl.q_off : q, ws + pl.k_off, fp8 ? ws + pl.v_off : v_new, k_pool,
+                         v_pool, num_pages, block_table, bt_stride, cu_seqlens_q,
+                         max_cache_len > 0 ? cache_seqlens : nullptr, total_q, max_seqlen_q, max_cache_len, out, lse,
+                         p.ws_bytes ? ws + pl.bytes : nullptr, workspace_bytes - pl.bytes, s);
   }
   if (append) {
     const csr::AppendArgs a = append_args(desc, batch, k_new, v_new, k_pool, v_pool, num_pages, block_table,
@@ -431,26 +460,25 @@ csr_status csr_prefill(const csr_attn_desc* desc, int32_t batch, const void* q, 
   Plan p;
   st = make_plan(desc, batch, total, max_seqlen, 0, p);
   if (st != CSR_OK) return st;
-  const size_t rope_bytes = rope_ws_bytes(desc, total);
-  if (rope_bytes + p.ws_bytes > 0) {
-    if (!workspace || workspace_bytes < rope_bytes + p.ws_bytes)
-      return fail(CSR_E_WORKSPACE, "workspace of %zu bytes required, got %zu", rope_bytes + p.ws_bytes,
+  const PrepLayout pl = prep_layout(desc, total);
+  if (pl.bytes + p.ws_bytes > 0) {
+    if (!workspace || workspace_bytes < pl.bytes + p.ws_bytes)
+      return fail(CSR_E_WORKSPACE, "workspace of %zu bytes required, got %zu", pl.bytes + p.ws_bytes,
                   workspace ? workspace_bytes : (size_t)0);
     if (!aligned16(workspace)) return fail(CSR_E_INVAL, "workspace must be 16-byte aligned");
   }
   hipStream_t s = static_cast<hipStream_t>(stream);
-  if (rope_bytes > 0) {
+  if (pl.bytes > 0) {
     char* ws = static_cast<char*>(workspace);
-    void* q_rot = ws;
-    void* k_rot = ws + rope_q_bytes(desc, total);
-    const csr::RopeArgs r = rope_args(desc, batch, q, k, v, q_rot, k_rot, write_cache ? k_pool : nullptr,
-                                      write_cache ? v_pool : nullptr, num_pages, block_table, bt_stride, cu_seqlens,
-                                      nullptr, total);
-    st = launched(csr::launch_rope_append(r, desc->dtype == CSR_BF16, s), "rope");
+    const bool rope = has_rope(desc), fp8 = kv_fp8(desc);
+    const csr::RopeArgs r = rope_args(desc, batch, q, k, v, ws + pl.q_off, ws + pl.k_off, ws + pl.v_off,
+                                      write_cache ? k_pool : nullptr, write_cache ? v_pool : nullptr, num_pages,
+                                      block_table, bt_stride, cu_seqlens, nullptr, total);
+    st = launched(csr::launch_rope_append(r, desc->dtype == CSR_BF16, s), "prep");
     if (st != CSR_OK) return st;
-    return run_attention(desc, batch, q_rot, k_rot, v, nullptr, nullptr, 0, nullptr, 1, cu_seqlens, nullptr, total,
-                         max_seqlen, 0, out, lse, p.ws_bytes ? ws + rope_bytes : nullptr, workspace_bytes - rope_bytes,
-                         s);
+    return run_attention(desc, batch, rope ? ws + pl.q_off : q, ws + pl.k_off, fp8 ? ws + pl.v_off : v, nullptr,
+                         nullptr, 0, nullptr, 1, cu_seqlens, nullptr, total, max_seqlen, 0, out, lse,
+                         p.ws_bytes ? ws + pl.bytes : nullptr, workspace_bytes - pl.bytes, s);
   }
   if (write_cache) {
     const csr::AppendArgs a = append_args(desc, batch, k, v, k_pool, v_pool, num_pages, block_table, bt_stride,

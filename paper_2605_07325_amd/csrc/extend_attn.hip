@@ -55,6 +55,8 @@ typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
 typedef short s16x4 __attribute__((ext_vector_type(4)));
 typedef __attribute__((address_space(3))) s16x4 lds_s16x4;
+typedef int32_t i32x2 __attribute__((ext_vector_type(2)));
+typedef __attribute__((address_space(3))) i32x2 lds_i32x2;
 
 
 constexpr int KT = 64;        // keys per tile
@@ -69,22 +71,48 @@ __device__ __forceinline__ int swz(int row) {
   else return ((row & 3) << 1) | ((row >> 2) & 1);
 }
 
+// Rows of fp8 keys (128 bytes at d = 128): each 16-lane group of a transposing
+// V read touches the 8 key rows {a, a+1, a+2, a+3, a+8, .., a+11}, which
+// differ in row bits 0, 1 and 3; the XOR uses exactly those bits (bit 2 folded
+// in) so the 8 rows land in 8 different chunk slots.
+__device__ __forceinline__ int swz8(int row) {
+  return ((row & 3) | ((row >> 1) & 4)) ^ ((row >> 2) & 1);
+}
+
 // Slot of 16-byte chunk c in key row `row` of an LDS tile: the row XOR plus,
 // for 256-byte rows, a swap of chunk bit 1 into bit 3 so the two 16-lane
 // groups of a transposing V read fall into opposite halves of the 64 banks.
 // A bijection on the chunks of each row; chunk_of_slot is its inverse.
-template <int NCH>
+template <int NCH, bool B8 = false>
 __device__ __forceinline__ int slot(int row, int c) {
+  if constexpr (B8) return c ^ swz8(row);
   int s = c ^ swz<NCH>(row);
   if constexpr (NCH == 16) s ^= ((c >> 1) & 1) << 3;
   return s;
 }
-template <int NCH>
+template <int NCH, bool B8 = false>
 __device__ __forceinline__ int chunk_of_slot(int row, int s) {
+  if constexpr (B8) return s ^ swz8(row);
   int c = s ^ swz<NCH>(row);
   if constexpr (NCH == 16) c ^= ((c >> 1) & 1) << 3;
   return c;
 }
+
+// Eight OCP e4m3 codes (bytes in memory order) as eight bf16 values: every
+// e4m3 value is exactly a bf16 value, so the conversion is exact.
+__device__ __forceinline__ u32x4 e4m3x8_to_bf16(u32x2 w) {
+  return u32x4{__builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8(w[0], 1.0f, false)),
+               __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8(w[0], 1.0f, true)),
+               __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8(w[1], 1.0f, false)),
+               __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8(w[1], 1.0f, true))};
+}
+
+// A K fragment as the MFMA's eight bf16 values: bf16 fragments as read, fp8
+// fragments (8 codes) converted.
+__device__ __forceinline__ u32x4 kfrag(u32x4 x) { return x; }
+__device__ __forceinline__ u32x4 kfrag(u32x2 x) { return e4m3x8_to_bf16(x); }
+template <bool B8> struct KFragT { typedef u32x4 type; };
+template <> struct KFragT<true> { typedef u32x2 type; };
 
 __device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
   f32x2 f = {lo, hi};
@@ -216,17 +244,20 @@ struct TileLoader {
 // Online softmax keeps a per-row reference max and rescales O only when a new
 // score exceeds it by more than 2^8 (wave-uniform branch); probabilities stay
 // below 2^8 and the final normalisation is exact whatever reference was used.
-template <int D, bool SCALAR_PAGES>
+template <int D, bool SCALAR_PAGES, bool KV8 = false>
 __global__ void __launch_bounds__(512, 1) attn_bf16_kernel(const AttnArgs a) {
+  static_assert(!KV8 || D == 128, "fp8 K/V rows are laid out for d = 128");
+  typedef typename KFragT<KV8>::type KF;  // one K fragment as read from LDS
   constexpr int NW = 8;
   constexpr int BM = NW * 32;
-  constexpr int ROWB = D * 2;
+  constexpr int ROWB = D * (KV8 ? 1 : 2);  // bytes per key row (bf16 or e4m3 codes)
   constexpr int NCH = ROWB / 16;
   constexpr int DS = D / 16;  // QK^T contraction steps
   constexpr int DB = D / 32;  // 32-wide d blocks of the output
   constexpr int TILEB = KT * ROWB;
   constexpr int ROWS_PER_KB = 1024 / ROWB;
   constexpr int NDMA = TILEB / (NW * 1024);  // DMA instructions per wave per tensor tile
+  static_assert(NDMA >= 1, "a tile must give every wave at least one DMA block");
   constexpr int ST = 4;                      // ring stages (K and V each)
   constexpr float THRESH = 8.f;              // lazy-rescale threshold (log2 units)
   __shared__ __attribute__((aligned(1024))) char lds[2 * ST * TILEB];
@@ -284,7 +315,7 @@ __global__ void __launch_bounds__(512, 1) attn_bf16_kernel(const AttnArgs a) {
 #pragma unroll
   for (int j = 0; j < NDMA; ++j) {
     drow[j] = (j * NW + wave) * ROWS_PER_KB + lane / NCH;
-    dchunk[j] = u.g * ROWB + (chunk_of_slot<NCH>(drow[j], lane % NCH) << 4);
+    dchunk[j] = u.g * ROWB + (chunk_of_slot<NCH, KV8>(drow[j], lane % NCH) << 4);
     pool_off[j] = (drow[j] & in_page_mask) * (a.Hkv * ROWB) + dchunk[j];
     new_off[j] = drow[j] * (a.Hkv * ROWB) + dchunk[j];
   }
@@ -358,7 +389,9 @@ __global__ void __launch_bounds__(512, 1) attn_bf16_kernel(const AttnArgs a) {
   // Per-lane LDS read offsets (stage and 32-key block offsets are added as immediates).
   int koff[DS];
 #pragma unroll
-  for (int ds = 0; ds < DS; ++ds) koff[ds] = l32 * ROWB + (slot<NCH>(l32, ds * 2 + h) << 4);
+  for (int ds = 0; ds < DS; ++ds)
+    koff[ds] = KV8 ? l32 * ROWB + (slot<NCH, true>(l32, ds) << 4) + 8 * h  // 8 codes: d = 16 ds + 8h ..
+                   : l32 * ROWB + (slot<NCH>(l32, ds * 2 + h) << 4);
   const int grp = lane >> 4, rr = (lane & 15) >> 2, qq = lane & 3, hh = grp >> 1;
   int voff_a[DB], voff_b[DB];
   {
@@ -372,6 +405,18 @@ __global__ void __launch_bounds__(512, 1) attn_bf16_kernel(const AttnArgs a) {
     }
   }
 
+  // fp8 V: one transposing byte read per (16-key half, 32-wide d block).  In a
+  // 16-lane group g, output lane i receives byte i % 8 of the reads of lanes
+  // 2k + i / 8 (k = 0 .. 7), so lane 2k + p points at key 8(k/4) + 4(g/2) + k%4
+  // (the probabilities' key order) and d column 16(g%2) + 8p of the block.
+  int voff8[DB];
+  if constexpr (KV8) {
+    const int g = lane >> 4, kk = (lane & 15) >> 1, p8 = lane & 1;
+    const int row = 8 * (kk >> 2) + 4 * (g >> 1) + (kk & 3);
+#pragma unroll
+    for (int db = 0; db < DB; ++db) voff8[db] = row * ROWB + (slot<NCH, true>(row, 2 * db + (g & 1)) << 4) + 8 * p8;
+  }
+
   f32x16 o[DB];
 #pragma unroll
   for (int db = 0; db < DB; ++db) o[db] = f32x16{};
@@ -382,23 +427,23 @@ __global__ void __launch_bounds__(512, 1) attn_bf16_kernel(const AttnArgs a) {
 
   // Scores of 32-key block kb of a K tile: S^T[key][row] (contraction steps [d0, d1)).
   // K fragments of k-steps [d0, d0 + DS/2) of block kb, and the score MFMAs over them.
-  auto load_k = [&](const char* kl, int kb, int d0, u32x4* kf) {
+  auto load_k = [&](const char* kl, int kb, int d0, KF* kf) {
 #pragma unroll
-    for (int i = 0; i < DS / 2; ++i) kf[i] = *reinterpret_cast<const u32x4*>(kl + kb * 32 * ROWB + koff[d0 + i]);
+    for (int i = 0; i < DS / 2; ++i) kf[i] = *reinterpret_cast<const KF*>(kl + kb * 32 * ROWB + koff[d0 + i]);
   };
-  auto mfma_k = [&](const u32x4* kf, int d0, f32x16& s) {
+  auto mfma_k = [&](const KF* kf, int d0, f32x16& s) {
 #pragma unroll
     for (int i = 0; i < DS / 2; ++i)
-      s = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, kf[i]), __builtin_bit_cast(bf16x8, qf[d0 + i]),
-                                                  s, 0, 0, 0);
+      s = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, kfrag(kf[i])),
+                                                  __builtin_bit_cast(bf16x8, qf[d0 + i]), s, 0, 0, 0);
   };
   auto qk = [&](const char* kl, int kb, f32x16& s) {
     s = f32x16{};
 #pragma unroll
     for (int ds = 0; ds < DS; ++ds) {
-      const u32x4 kf = *reinterpret_cast<const u32x4*>(kl + kb * 32 * ROWB + koff[ds]);
-      s = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, kf), __builtin_bit_cast(bf16x8, qf[ds]),
-                                                  s, 0, 0, 0);
+      const KF kf = *reinterpret_cast<const KF*>(kl + kb * 32 * ROWB + koff[ds]);
+      s = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, kfrag(kf)),
+                                                  __builtin_bit_cast(bf16x8, qf[ds]), s, 0, 0, 0);
     }
   };
   // O^T += V^T P^T for 32-key block kb.  Contraction slot 8h+s of half hf is
@@ -407,6 +452,15 @@ __global__ void __launch_bounds__(512, 1) attn_bf16_kernel(const AttnArgs a) {
 #pragma unroll
     for (int hf = 0; hf < 2; ++hf) {
       const char* vb = vl + (kb * 32 + 16 * hf) * ROWB;
+      if constexpr (KV8) {
+#pragma unroll
+        for (int db = 0; db < DB; ++db) {
+          const u32x2 w = __builtin_bit_cast(u32x2, __builtin_amdgcn_ds_read_tr8_b64_v2i32((lds_i32x2*)(vb + voff8[db])));
+          o[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, e4m3x8_to_bf16(w)),
+                                                          __builtin_bit_cast(bf16x8, pf[hf]), o[db], 0, 0, 0);
+        }
+        continue;
+      }
 #pragma unroll
       for (int db = 0; db < DB; ++db) {
         const u32x2 wa = __builtin_bit_cast(u32x2, __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4*)(vb + voff_a[db])));
@@ -425,6 +479,25 @@ __global__ void __launch_bounds__(512, 1) attn_bf16_kernel(const AttnArgs a) {
   auto pv_asm = [&](auto voff_c, const u32x4* pf) {
     constexpr int VOFF = decltype(voff_c)::value;
     static_assert(VOFF + 16 * ROWB < 65536, "DS immediate offset range");
+    if constexpr (KV8) {
+      static_assert(DB == 4, "fp8 V path is laid out for d = 128");
+      u32x2 w8[2][DB];
+#pragma unroll
+      for (int hf = 0; hf < 2; ++hf)
+#pragma unroll
+        for (int db = 0; db < DB; ++db)
+          asm volatile("ds_read_b64_tr_b8 %0, %1 offset:%2" : "=v"(w8[hf][db]) : "v"(vring_addr + voff8[db]), "i"(VOFF + hf * 16 * ROWB));
+      asm volatile("s_waitcnt lgkmcnt(0)"
+                   : "+v"(w8[0][0]), "+v"(w8[0][1]), "+v"(w8[0][2]), "+v"(w8[0][3]), "+v"(w8[1][0]), "+v"(w8[1][1]),
+                     "+v"(w8[1][2]), "+v"(w8[1][3]));
+#pragma unroll
+      for (int hf = 0; hf < 2; ++hf)
+#pragma unroll
+        for (int db = 0; db < DB; ++db)
+          o[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, e4m3x8_to_bf16(w8[hf][db])),
+                                                          __builtin_bit_cast(bf16x8, pf[hf]), o[db], 0, 0, 0);
+      return;
+    }
     u32x2 w[2][DB][2];
 #pragma unroll
     for (int hf = 0; hf < 2; ++hf)
@@ -503,11 +576,11 @@ __global__ void __launch_bounds__(512, 1) attn_bf16_kernel(const AttnArgs a) {
   // instead of arriving with every other wave's at the tile boundary.
   // K fragments of the first half of the next step's score block, read one
   // group of products ahead so that their LDS latency hides behind MFMAs.
-  u32x4 kpre[DS / 2];
+  KF kpre[DS / 2];
   auto step = [&](f32x16& s_cur, f32x16& s_next, auto voff_c, const char* kl_next, int kb_next,
                   const char* kl_after, int kb_after, auto dma_a, auto dma_b) {
     u32x4 pf[2];
-    u32x4 kh1[DS / 2];
+    KF kh1[DS / 2];
     s_next = f32x16{};
     load_k(kl_next, kb_next, DS / 2, kh1);
     __builtin_amdgcn_sched_barrier(0);
@@ -647,7 +720,8 @@ __global__ void __launch_bounds__(512, 1) attn_bf16_kernel(const AttnArgs a) {
   const float lsum = __uint_as_float(pr[0]) + __uint_as_float(pr[1]);
   if (!valid) return;
   const int64_t qrow = (int64_t)(u.cuq + tok) * a.Hq + u.g * G + (m_row - tok * G);
-  const float inv = lsum > 0.f ? 1.f / lsum : 0.f;
+  // (an fp8 cache stores V / v_scale: the scale comes back here)
+  const float inv = (lsum > 0.f ? 1.f / lsum : 0.f) * a.v_scale;
   const float lse = lsum > 0.f ? (mref + __log2f(lsum)) * LN2 : -INFINITY;
   if (a.nsplit == 1) {
     char* orow = static_cast<char*>(a.out) + qrow * D * 2;
@@ -834,7 +908,11 @@ hipError_t launch_attention(const AttnArgs& a, int dtype_bf16, hipStream_t strea
   if (a.n_units == 0) return hipSuccess;
   unsigned grid = (unsigned)a.n_units;
   if (a.xcd_remap) grid = (grid + 7u) & ~7u;
-  if (dtype_bf16) {
+  if (dtype_bf16 && a.kv_fp8) {
+    // fp8 rows: 8 keys per DMA block
+    if (a.P >= 8) hipLaunchKernelGGL((attn_bf16_kernel<128, true, true>), dim3(grid), dim3(512), 0, stream, a);
+    else hipLaunchKernelGGL((attn_bf16_kernel<128, false, true>), dim3(grid), dim3(512), 0, stream, a);
+  } else if (dtype_bf16) {
     // Scalar page-id loads need every DMA block (4 keys at d=128, 8 at d=64) inside one page.
     const bool scalar_pages = a.P >= (a.d == 128 ? 4 : 8);
     if (a.d == 128) {

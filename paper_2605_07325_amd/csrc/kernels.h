@@ -24,7 +24,9 @@ struct AttnArgs {
   int32_t num_pages;
   int32_t bt_stride;
   int32_t Hq, Hkv, G, d, P, log2P;
-  float scale_log2;          // softmax scale * log2(e)
+  float scale_log2;          // softmax scale * log2(e) (times k_scale for an fp8 cache)
+  float v_scale;             // output multiplier: 1, or v_scale for an fp8 cache
+  int32_t kv_fp8;            // K/V (pool and chunk) are OCP e4m3 codes (bf16 q, d = 128)
   int32_t batch, total_q;
   int32_t mtiles;            // packed-row tiles per (sequence, kv head)
   int32_t nsplit;            // key-range splits per tile
@@ -58,21 +60,25 @@ struct AppendArgs {
 };
 hipError_t launch_append(const AppendArgs& a, hipStream_t stream);
 
-// Rotary embedding at absolute positions L_b + i, fused with the append.
+// Rotary embedding at absolute positions L_b + i and/or fp8 quantisation of
+// K/V, fused with the append.
 struct RopeArgs {
   const void* q;             // [T_q][Hq][d] or nullptr (keys only)
   const void* k;             // [T_q][Hkv][d]
   const void* v;             // [T_q][Hkv][d], read only when k_pool is set
   void* q_out;               // rotated q, or nullptr
-  void* k_out;               // rotated k, or nullptr
+  void* k_out;               // rotated (and, kv8, quantised) k, or nullptr
+  void* v_out;               // kv8: quantised v, or nullptr
   void* k_pool;              // nullptr: no cache write
   void* v_pool;
   const int32_t* block_table;
   const int32_t* cu_q;
   const int32_t* cache_len;  // nullptr: every L_b = 0
   int32_t num_pages, bt_stride, batch, total_q, Hq, Hkv, d, log2P;
-  int32_t rdim;              // rotated dims, multiple of 16, <= d
-  int32_t style;             // 1 neox (i, i + r/2), 2 interleaved (2i, 2i + 1)
+  int32_t rdim;              // rotated dims, multiple of 16, <= d (0: no rotation)
+  int32_t style;             // 0 none, 1 neox (i, i + r/2), 2 interleaved (2i, 2i + 1)
+  int32_t kv8;               // keys/values (outputs and cache) are e4m3 codes; bf16 inputs
+  float inv_k, inv_v;        // fp32(1 / k_scale), fp32(1 / v_scale)
   double half_turns[64];     // theta_i / pi for i < rdim / 2
 };
 hipError_t launch_rope_append(const RopeArgs& a, int dtype_bf16, hipStream_t stream);

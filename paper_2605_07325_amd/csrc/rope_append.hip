@@ -1,5 +1,11 @@
 // Rotary position embedding (RoFormer, Su et al. 2021) at absolute cache
-// positions, fused with the paged KV append.
+// positions and FP8 (OCP e4m3) quantisation of the K/V cache, fused with the
+// paged KV append.
+//
+// With an fp8 cache each key (after its rotation) and value is stored as
+// e4m3(clamp(x * inv_scale, +-448)), nearest even, inv_scale = fp32(1/scale);
+// the quantised chunk rows also go to the workspace, so the attention reads a
+// chunk key exactly as later calls will read it from the cache.
 //
 // Chunk row i of sequence b sits at position pos = L_b + i, fixed for as long
 // as the row stays cached (prefix stability, Theorem 1), so its query and key
@@ -27,6 +33,7 @@ namespace csr {
 namespace {
 
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
 typedef float f32x2 __attribute__((ext_vector_type(2)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
@@ -83,6 +90,27 @@ __device__ __forceinline__ void store8(void* base, int64_t e, const float (&y)[8
   }
 }
 
+// OCP e4m3 code of x: saturate to +-448, round to nearest even (subnormal
+// steps of 2^-9), NaN to 0x7f.  Rounds the fp32 bit pattern at the 3-bit
+// mantissa (a carry moves the exponent up, which is the correct result).
+__device__ __forceinline__ uint32_t e4m3_code(float x) {
+  if (x != x) return 0x7f;
+  const uint32_t sign = (__float_as_uint(x) >> 24) & 0x80;
+  const float a = fminf(fabsf(x), 448.f);
+  if (a < 0.015625f) return sign | (uint32_t)rintf(a * 512.f);  // exact scaling; 8 = smallest normal
+  const uint32_t b = __float_as_uint(a);
+  const uint32_t r = b + 0x7FFFFu + ((b >> 20) & 1u);
+  return sign | (((r >> 23) - 120u) << 3) | ((r >> 20) & 7u);
+}
+
+// 8 values scaled by inv and quantised, stored as 8 bytes.
+__device__ __forceinline__ void store8q(void* base, int64_t e, const float (&y)[8], float inv) {
+  uint32_t w[2] = {0, 0};
+#pragma unroll
+  for (int j = 0; j < 8; ++j) w[j >> 2] |= e4m3_code(y[j] * inv) << (8 * (j & 3));
+  *reinterpret_cast<u32x2*>(static_cast<uint8_t*>(base) + e) = u32x2{w[0], w[1]};
+}
+
 // Bit copy of 8 elements (tail dims, value rows).
 template <bool BF16>
 __device__ __forceinline__ void copy8(void* dst, const void* src, int64_t de, int64_t se) {
@@ -93,15 +121,23 @@ __device__ __forceinline__ void copy8(void* dst, const void* src, int64_t de, in
   for (int j = 0; j < kWords; ++j) d[j] = s[j];
 }
 
-template <bool BF16>
+template <bool BF16, bool KV8>
 __device__ __forceinline__ void rotate_piece(const RopeArgs& a, const f32x2* cs, int tok, int64_t slot, int u,
                                              int rot_units, int per_row, int n_rot, int nq, bool neox) {
   const int d = a.d;
   const int half = a.rdim >> 1;
-  if (u >= rot_units) {  // value row piece: bit copy into the cache
+  if (u >= rot_units) {  // value row piece: into the cache (and, quantised, the workspace)
     const int w = u - rot_units;
     const int g = w / (d >> 3), e = (w - g * (d >> 3)) << 3;
-    copy8<BF16>(a.v_pool, a.v, (slot * a.Hkv + g) * d + e, ((int64_t)tok * a.Hkv + g) * d + e);
+    const int64_t src = ((int64_t)tok * a.Hkv + g) * d + e;
+    if constexpr (KV8) {
+      float x[8];
+      load8<BF16>(a.v, src, x);
+      if (a.v_out) store8q(a.v_out, src, x, a.inv_v);
+      if (slot >= 0) store8q(a.v_pool, (slot * a.Hkv + g) * d + e, x, a.inv_v);
+    } else {
+      copy8<BF16>(a.v_pool, a.v, (slot * a.Hkv + g) * d + e, src);
+    }
     return;
   }
   const int r = u / per_row, piece = u - r * per_row;
@@ -112,10 +148,22 @@ __device__ __forceinline__ void rotate_piece(const RopeArgs& a, const f32x2* cs,
   void* out = is_q ? a.q_out : a.k_out;
   void* pool = is_q ? nullptr : (slot >= 0 ? a.k_pool : nullptr);
   const int64_t prow = is_q ? 0 : (slot * a.Hkv + h) * d;
-  if (piece >= n_rot) {  // dims >= r: unchanged
+  const bool quant = KV8 && !is_q;  // keys of an fp8 cache are stored as codes
+  auto put = [&](void* base, int64_t e, const float (&y)[8]) {
+    if (quant) store8q(base, e, y, a.inv_k);
+    else store8<BF16>(base, e, y);
+  };
+  if (piece >= n_rot) {  // dims >= r: unchanged (quantised for an fp8 cache)
     const int e = a.rdim + ((piece - n_rot) << 3);
-    if (out) copy8<BF16>(out, src, row + e, row + e);
-    if (pool) copy8<BF16>(pool, src, prow + e, row + e);
+    if (quant) {
+      float x[8];
+      load8<BF16>(src, row + e, x);
+      if (out) put(out, row + e, x);
+      if (pool) put(pool, prow + e, x);
+    } else {
+      if (out) copy8<BF16>(out, src, row + e, row + e);
+      if (pool) copy8<BF16>(pool, src, prow + e, row + e);
+    }
     return;
   }
   if (neox) {
@@ -130,12 +178,12 @@ __device__ __forceinline__ void rotate_piece(const RopeArgs& a, const f32x2* cs,
       y1[j] = fmaf(x1[j], t[0], x0[j] * t[1]);
     }
     if (out) {
-      store8<BF16>(out, row + e0, y0);
-      store8<BF16>(out, row + e1, y1);
+      put(out, row + e0, y0);
+      put(out, row + e1, y1);
     }
     if (pool) {
-      store8<BF16>(pool, prow + e0, y0);
-      store8<BF16>(pool, prow + e1, y1);
+      put(pool, prow + e0, y0);
+      put(pool, prow + e1, y1);
     }
   } else {
     const int e0 = piece << 3;
@@ -147,12 +195,12 @@ __device__ __forceinline__ void rotate_piece(const RopeArgs& a, const f32x2* cs,
       y[2 * j] = fmaf(x[2 * j], t[0], -x[2 * j + 1] * t[1]);
       y[2 * j + 1] = fmaf(x[2 * j + 1], t[0], x[2 * j] * t[1]);
     }
-    if (out) store8<BF16>(out, row + e0, y);
-    if (pool) store8<BF16>(pool, prow + e0, y);
+    if (out) put(out, row + e0, y);
+    if (pool) put(pool, prow + e0, y);
   }
 }
 
-template <bool BF16>
+template <bool BF16, bool KV8>
 __global__ void __launch_bounds__(256) rope_append_kernel(RopeArgs a) {
   __shared__ f32x2 cs[64];
   const int tok = blockIdx.x;
@@ -184,10 +232,10 @@ __global__ void __launch_bounds__(256) rope_append_kernel(RopeArgs a) {
   const int nq = a.q ? a.Hq : 0;
   const int rows = nq + a.Hkv;
   const int rot_units = rows * per_row;
-  const int v_units = slot >= 0 ? a.Hkv * (d >> 3) : 0;
+  const int v_units = (slot >= 0 || (KV8 && a.v_out)) ? a.Hkv * (d >> 3) : 0;
 
   for (int u = blockIdx.y * blockDim.x + threadIdx.x; u < rot_units + v_units; u += gridDim.y * blockDim.x)
-    rotate_piece<BF16>(a, cs, tok, slot, u, rot_units, per_row, n_rot, nq, neox);
+    rotate_piece<BF16, KV8>(a, cs, tok, slot, u, rot_units, per_row, n_rot, nq, neox);
 }
 
 }  // namespace
@@ -196,15 +244,17 @@ hipError_t launch_rope_append(const RopeArgs& a, int dtype_bf16, hipStream_t str
   if (a.total_q == 0) return hipSuccess;
   // Upper bound of the pieces one token has (rows * pieces per row + value pieces).
   const int pieces_per_row = (a.style == 1 ? a.rdim / 16 : a.rdim / 8) + (a.d - a.rdim) / 8;
-  const int units = ((a.q ? a.Hq : 0) + a.Hkv) * pieces_per_row + (a.k_pool ? a.Hkv * (a.d / 8) : 0);
+  const bool v_rows = a.k_pool || (a.kv8 && a.v_out);
+  const int units = ((a.q ? a.Hq : 0) + a.Hkv) * pieces_per_row + (v_rows ? a.Hkv * (a.d / 8) : 0);
   // Slices per token: enough workgroups (~2048) to spread a short chunk over
   // the chip, one when the chunk alone provides them.
   const int max_slices = (units + 255) / 256;
   int slices = (2048 + a.total_q - 1) / a.total_q;
   if (slices > max_slices) slices = max_slices;
   const dim3 grid((unsigned)a.total_q, (unsigned)slices);
-  if (dtype_bf16) hipLaunchKernelGGL(rope_append_kernel<true>, grid, dim3(256), 0, stream, a);
-  else hipLaunchKernelGGL(rope_append_kernel<false>, grid, dim3(256), 0, stream, a);
+  if (a.kv8) hipLaunchKernelGGL((rope_append_kernel<true, true>), grid, dim3(256), 0, stream, a);
+  else if (dtype_bf16) hipLaunchKernelGGL((rope_append_kernel<true, false>), grid, dim3(256), 0, stream, a);
+  else hipLaunchKernelGGL((rope_append_kernel<false, false>), grid, dim3(256), 0, stream, a);
   return hipGetLastError();
 }
 

@@ -6,6 +6,7 @@ import os
 import re
 
 import pytest
+import torch
 
 from paper_2605_07325_amd import csr
 
@@ -173,3 +174,27 @@ def test_rope_workspace_holds_rotated_q_and_k():
                                                         16, 100) - 16)
     assert need > 0 and st == csr.CSR_E_WORKSPACE
     assert call_extend(good_desc(rope_style=csr.CSR_ROPE_NEOX, rope_theta=1e4), ws=None) == csr.CSR_E_WORKSPACE
+
+
+@pytest.mark.parametrize("over,code", [
+    (dict(kv_dtype=7, k_scale=1.0, v_scale=1.0), csr.CSR_E_INVAL),                        # unknown cache type
+    (dict(kv_dtype=csr.CSR_KV_FP8_E4M3, k_scale=0.0, v_scale=1.0), csr.CSR_E_INVAL),       # no key scale
+    (dict(kv_dtype=csr.CSR_KV_FP8_E4M3, k_scale=1.0, v_scale=float("nan")), csr.CSR_E_INVAL),
+    (dict(kv_dtype=csr.CSR_KV_FP8_E4M3, k_scale=1.0, v_scale=1.0, head_dim=64), csr.CSR_E_UNSUPPORTED),
+    (dict(kv_dtype=csr.CSR_KV_FP8_E4M3, k_scale=1.0, v_scale=1.0, dtype=torch.float32), csr.CSR_E_UNSUPPORTED),
+])
+def test_fp8_cache_descriptor_validation(over, code):
+    assert call_extend(good_desc(**over)) == code
+    assert csr.lib().csr_last_error().decode()
+
+
+def test_fp8_cache_workspace_holds_quantised_chunk():
+    plain = good_desc(num_q_heads=64, num_kv_heads=4)
+    fp8 = good_desc(num_q_heads=64, num_kv_heads=4, kv_dtype=csr.CSR_KV_FP8_E4M3, k_scale=0.05, v_scale=0.05)
+    both = good_desc(num_q_heads=64, num_kv_heads=4, kv_dtype=csr.CSR_KV_FP8_E4M3, k_scale=0.05, v_scale=0.05,
+                     rope_style=csr.CSR_ROPE_NEOX, rope_theta=1e6)
+    align = lambda x: (x + 255) // 256 * 256  # noqa: E731
+    for T, L in ((512, 122880), (1, 122880), (7, 0)):
+        base = csr.extend_workspace_size(plain, 1, T, T, L)
+        assert csr.extend_workspace_size(fp8, 1, T, T, L) - base == 2 * align(T * 4 * 128)
+        assert csr.extend_workspace_size(both, 1, T, T, L) - base == align(T * 64 * 128 * 2) + 2 * align(T * 4 * 128)

@@ -1,0 +1,185 @@
+"""GPU parity for the FP8 (OCP e4m3) KV cache.
+
+The cache holds e4m3 codes with per-tensor scales; the chunk's bf16 keys and
+values are quantised by the fused prep launch (and appended); the attention
+converts codes to bf16 exactly and computes as the bf16 path does.  The
+oracle evaluates the same definition in fp64 (codes decoded exactly, chunk
+quantised by its own encoder), so outputs meet the bf16 gates and appended
+codes are compared bit for bit (with RoPE the rotation is fp32 on the GPU and
+fp64 in the oracle, so a code may rarely sit one step away).
+"""
+import os
+
+import numpy as np
+import pytest
+import torch
+
+from oracle import oracle
+from paper_2605_07325_amd import csr
+from paper_2605_07325_amd import datagen as dg
+from tests.gpu_harness import Dev, compare, note, values
+
+pytestmark = pytest.mark.gpu
+
+KS, VS = 0.0625, 0.0390625
+
+
+@pytest.fixture(autouse=True)
+def _no_split_override():
+    saved = os.environ.pop("CSR_NSPLIT", None)
+    yield
+    os.environ.pop("CSR_NSPLIT", None)
+    if saved is not None:
+        os.environ["CSR_NSPLIT"] = saved
+
+
+class Dev8(Dev):
+    """Device copies of an fp8-cache case (uint8 pools) and its descriptor."""
+
+    def __init__(self, case, rope=None):
+        super().__init__(case)
+        self.k_pool = torch.from_numpy(case.k_pool).cuda()
+        self.v_pool = torch.from_numpy(case.v_pool).cuda()
+        self.desc.kv_dtype = csr.CSR_KV_FP8_E4M3
+        self.desc.k_scale, self.desc.v_scale = KS, VS
+        if rope is not None:
+            self.desc.rope_style, self.desc.rope_dim, self.desc.rope_theta = rope
+
+
+def fp8_case(label, cfg_id, **kw):
+    return dg.with_fp8_pools(dg.make_case(label, dtype=dg.BF16, head_dim=128, seed=3, cfg_id=cfg_id, **kw),
+                             cfg_id=cfg_id)
+
+
+def oracle8(case, rows, rope=None, prefill=False):
+    out, lse, _ = oracle.attention(oracle.BF16, case.q, case.k_new, case.v_new, case.k_pool, case.v_pool,
+                                   case.block_table, case.bt_stride, case.cu_seqlens_q,
+                                   None if prefill else case.cache_len, rows, case.num_q_heads, case.num_kv_heads,
+                                   case.head_dim, case.page_size, rope=rope, fp8=(KS, VS))
+    return out, lse
+
+
+def check_pool8(case, dev, cache_len, rope=None):
+    kp, vp = oracle.kv_append(case.k_new, case.v_new, case.k_pool, case.v_pool, case.block_table, case.bt_stride,
+                              case.cu_seqlens_q, cache_len, case.num_kv_heads, case.head_dim, case.page_size,
+                              rope=rope, fp8=(KS, VS))
+    gk, gv = dev.k_pool.cpu().numpy(), dev.v_pool.cpu().numpy()
+    assert np.array_equal(gv, vp), "values (and every untouched byte) must match bit for bit"
+    if rope is None:
+        assert np.array_equal(gk, kp)
+        note("fp8 pool: codes bit for bit")
+        return
+    diff = np.nonzero(gk != kp)
+    steps = np.abs(oracle.e4m3_decode(gk[diff]) - oracle.e4m3_decode(kp[diff]))
+    nxt = np.abs(oracle.e4m3_decode(kp[diff]))
+    # one code step (relative 2^-3, or the subnormal step 2^-9) at most, and rarely
+    assert np.all(steps <= np.maximum(nxt * 2.0 ** -3, 2.0 ** -9) * (1 + 1e-12))
+    assert len(diff[0]) <= max(4, gk.size // 10000)
+    note(f"fp8 pool with RoPE: {len(diff[0])} codes one step from the oracle's")
+
+
+SMALL = [
+    ("g16_L1000", dict(num_q_heads=32, num_kv_heads=2, cache_len=[1000], seqlen_q=[37], page_size=16, scale=0.5)),
+    ("ragged_empty", dict(num_q_heads=16, num_kv_heads=2, cache_len=[0, 513, 64, 2049, 300], seqlen_q=[17, 1, 0, 64, 9],
+                          page_size=16, scale=0.5, interleave=True)),
+    ("page4", dict(num_q_heads=8, num_kv_heads=1, cache_len=[777], seqlen_q=[100], page_size=4, scale=0.5)),
+    ("prefill_L0", dict(num_q_heads=16, num_kv_heads=4, cache_len=[0], seqlen_q=[300], page_size=16, scale=0.5)),
+    ("decode_n1", dict(num_q_heads=16, num_kv_heads=1, cache_len=[5000], seqlen_q=[1], page_size=16, scale=0.5)),
+]
+
+
+@pytest.mark.parametrize("label,kw", SMALL, ids=[s[0] for s in SMALL])
+@pytest.mark.parametrize("nsplit", [None, 3])
+def test_fp8_extend_append_all_rows(label, kw, nsplit):
+    if nsplit:
+        os.environ["CSR_NSPLIT"] = str(nsplit)
+    case = fp8_case(label, 600, **kw)
+    note(f"fp8 {label} nsplit={nsplit} L={case.cache_len.tolist()} n={case.seqlen_q.tolist()}: "
+         "csr_extend_attention(APPEND)")
+    dev = Dev8(case)
+    out, lse = dev.extend(append=True)
+    torch.cuda.synchronize()
+    rows = np.arange(case.total_q, dtype=np.int32)
+    ref, ref_lse = oracle8(case, rows)
+    compare(case, out, lse, rows, ref, ref_lse, f"fp8/{label}/split={nsplit}")
+    check_pool8(case, dev, case.cache_len)
+
+
+def test_fp8_kv_append_alone():
+    case = fp8_case("append", 601, num_q_heads=16, num_kv_heads=2, cache_len=[40, 700], seqlen_q=[70, 5],
+                    page_size=16, scale=0.5, interleave=True)
+    note("fp8 csr_kv_append")
+    dev = Dev8(case)
+    dev.append()
+    torch.cuda.synchronize()
+    check_pool8(case, dev, case.cache_len)
+
+
+@pytest.mark.parametrize("style", [csr.CSR_ROPE_NEOX, csr.CSR_ROPE_INTERLEAVED])
+def test_fp8_with_rope(style):
+    case = fp8_case("rope8", 602, num_q_heads=16, num_kv_heads=2, cache_len=[3000], seqlen_q=[90], page_size=16,
+                    scale=0.5)
+    rope = (style, 0, 1e6)
+    note(f"fp8 + rope style {style}: csr_extend_attention(APPEND)")
+    dev = Dev8(case, rope)
+    out, lse = dev.extend(append=True)
+    torch.cuda.synchronize()
+    rows = np.arange(case.total_q, dtype=np.int32)
+    ref, ref_lse = oracle8(case, rows, rope=rope)
+    compare(case, out, lse, rows, ref, ref_lse, f"fp8/rope{style}")
+    check_pool8(case, dev, case.cache_len, rope=rope)
+
+
+@pytest.mark.parametrize("n", [512, 1])
+def test_fp8_c3_120k_prefix(n):
+    base = dg.config(f"c3_{n}")
+    case = dg.with_fp8_pools(base, cfg_id=603)
+    note(f"fp8 c3 L=122880 n={n}: csr_extend_attention(APPEND)")
+    dev = Dev8(case)
+    out, lse = dev.extend(append=True)
+    torch.cuda.synchronize()
+    rows = dg.sample_rows(case, 64, cfg_id=3)
+    ref, ref_lse = oracle8(case, rows)
+    compare(case, out, lse, rows, ref, ref_lse, f"fp8/c3_{n}")
+    check_pool8(case, dev, case.cache_len)
+
+
+def test_fp8_chunk_split_on_device():
+    """extend(L, n1) + append, then extend(L + n1, n2) over that cache, equals
+    extend(L, n1 + n2): a chunk key is quantised once, the same both ways."""
+    L, n1, n2 = 2500, 120, 77
+    kw = dict(num_q_heads=16, num_kv_heads=2, page_size=16, scale=0.5)
+    one = fp8_case("one8", 604, cache_len=[L], seqlen_q=[n1 + n2], **kw)
+    note(f"fp8 chunk split L={L} n={n1}+{n2}")
+    dev_one = Dev8(one)
+    out_one, lse_one = dev_one.extend()
+    a = fp8_case("one8", 604, cache_len=[L], seqlen_q=[n1], **kw)
+    for f in ("q", "k_new", "v_new"):
+        getattr(a, f)[:] = getattr(one, f)[:n1]
+    a.k_pool, a.v_pool, a.block_table, a.bt_stride = one.k_pool, one.v_pool, one.block_table, one.bt_stride
+    dev_a = Dev8(a)
+    out_a, _ = dev_a.extend(append=True)
+    b = fp8_case("one8", 604, cache_len=[L + n1], seqlen_q=[n2], **kw)
+    for f in ("q", "k_new", "v_new"):
+        getattr(b, f)[:] = getattr(one, f)[n1:]
+    b.block_table, b.bt_stride = one.block_table, one.bt_stride
+    dev_b = Dev8(b)
+    dev_b.k_pool, dev_b.v_pool = dev_a.k_pool, dev_a.v_pool
+    out_b, lse_b = dev_b.extend()
+    torch.cuda.synchronize()
+    assert np.abs(values(a, out_a) - values(one, out_one)[:n1]).max() < 1e-2
+    assert np.abs(values(b, out_b) - values(one, out_one)[n1:]).max() < 1e-2
+    assert np.abs(lse_b.cpu().numpy() - lse_one.cpu().numpy()[n1:]).max() < 1e-4
+
+
+def test_fp8_prefill_writes_the_quantised_cache():
+    case = fp8_case("pf8", 605, num_q_heads=16, num_kv_heads=2, cache_len=[0], seqlen_q=[2600], page_size=16,
+                    scale=0.5)
+    note("fp8 csr_prefill with cache write")
+    dev = Dev8(case)
+    out, lse = dev.prefill(write_cache=True)
+    torch.cuda.synchronize()
+    rows = dg.sample_rows(case, 48, cfg_id=6)
+    ref, ref_lse = oracle8(case, rows, prefill=True)
+    compare(case, out, lse, rows, ref, ref_lse, "fp8/prefill")
+    check_pool8(case, dev, None)
