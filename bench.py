@@ -286,6 +286,9 @@ def main():
                     help="rotate q and k_new at their absolute positions inside the step (fused with the append)")
     ap.add_argument("--rope-theta", type=float, default=1e6)
     ap.add_argument("--rope-dim", type=int, default=0, help="rotated dims (0 = head_dim)")
+    ap.add_argument("--kv", choices=("same", "fp8"), default="same",
+                    help="fp8: the cache holds OCP e4m3 codes (k_scale 0.0625, v_scale 0.0390625); the chunk is "
+                         "quantised inside the step")
     ap.add_argument("--asr-period-ms", type=float, default=2.0, help="asr: task arrival period")
     ap.add_argument("--asr-secondary-cus-per-xcd", type=int, default=8, help="asr: secondary partition size")
     ap.add_argument("--asr-tau", type=int, default=110000, help="asr: eviction threshold tau_mem (tokens)")
@@ -320,6 +323,10 @@ def main():
 
     t0 = time.perf_counter()
     case = dg.config(args.workload)
+    fp8 = args.kv == "fp8"
+    if fp8:
+        case = dg.with_fp8_pools(case, cfg_id=603)   # random e4m3 codes for the cached prefix
+    wl_name = args.workload + ("_fp8" if fp8 else "")
     log(f"workload {args.workload}: L={case.cache_len.tolist()} n={case.seqlen_q.tolist()} "
         f"Hq={case.num_q_heads} Hkv={case.num_kv_heads} d={case.head_dim} P={case.page_size} "
         f"({time.perf_counter() - t0:.1f}s to generate)")
@@ -332,7 +339,8 @@ def main():
         return torch.from_numpy(np.ascontiguousarray(a)).cuda()
 
     q, k_new, v_new = dev(case.q), dev(case.k_new), dev(case.v_new)
-    pools = [(dev(case.k_pool), dev(case.v_pool))]
+    pools = [((torch.from_numpy(case.k_pool).cuda(), torch.from_numpy(case.v_pool).cuda()) if fp8
+              else (dev(case.k_pool), dev(case.v_pool)))]
     for _ in range(max(1, args.pools) - 1):
         pools.append((pools[0][0].clone(), pools[0][1].clone()))
     bt = None if case.block_table is None else torch.from_numpy(case.block_table).cuda()
@@ -343,7 +351,11 @@ def main():
                                torch.bfloat16 if bf16 else torch.float32)
     desc = csr.make_desc(case.num_q_heads, case.num_kv_heads, case.head_dim, case.page_size,
                          torch.bfloat16 if bf16 else torch.float32, rope_style=rope_style, rope_dim=args.rope_dim,
-                         rope_theta=args.rope_theta if rope_style else 0.0)
+                         rope_theta=args.rope_theta if rope_style else 0.0,
+                         kv_dtype=csr.CSR_KV_FP8_E4M3 if fp8 else csr.CSR_KV_SAME,
+                         k_scale=0.0625 if fp8 else 0.0, v_scale=0.0390625 if fp8 else 0.0)
+    if fp8:  # the unrotated comparison keeps the fp8 cache
+        plain_desc.kv_dtype, plain_desc.k_scale, plain_desc.v_scale = csr.CSR_KV_FP8_E4M3, 0.0625, 0.0390625
     out = torch.empty_like(q)
     lse = torch.empty((case.total_q, case.num_q_heads), dtype=torch.float32, device="cuda")
     if prefill_mode:
@@ -399,8 +411,8 @@ def main():
     achieved = flops / (attn_avg * 1e-3) / 1e12
     log(f"{args.steps} steps: {ms_per_step:.4f} ms/step ({value:.1f} TFLOP/s); attention kernel avg "
         f"{attn_avg:.4f} ms (min {min(attn_ms):.4f}) = {achieved:.1f} TFLOP/s = {100 * achieved / peak:.1f}% of peak")
-    abytes = case.algorithmic_bytes(append=True)
-    traffic = measured_traffic(args.workload)
+    abytes = case.algorithmic_bytes(append=True, kv_bytes=1 if fp8 else None)
+    traffic = measured_traffic(wl_name)
     rec = {
         "metric": "extend-attn TFLOP/s & ms/layer at 120K cached prefix, 512-tok chunk; % MFMA peak",
         "value": round(value, 3),
@@ -419,7 +431,8 @@ def main():
                          f"prefix, n={case.max_seqlen_q} chunk, batch {case.batch}, GQA {case.num_q_heads}q/"
                          f"{case.num_kv_heads}kv, head_dim {case.head_dim}, page {case.page_size}, "
                          f"{'kv append + ' if not prefill_mode else 'cache write + '}attention (+ split-K merge)"),
-            "name": args.workload,
+            "name": wl_name,
+            "kv_cache": "fp8 e4m3, per-tensor scales (k 0.0625, v 0.0390625)" if fp8 else "input type",
             "global_batch": case.batch,
             "seq_len": int(case.max_cache_len + case.max_seqlen_q),
             "chunk_tokens": case.total_q,
@@ -434,7 +447,7 @@ def main():
             "unit": "TFLOP/s",
             "frac": round(achieved / peak, 4),
             "traffic": traffic,
-            "kernel": "attn_bf16_kernel" if bf16 else "attn_f32_kernel",
+            "kernel": ("attn_bf16_kernel<fp8 K/V>" if fp8 else "attn_bf16_kernel") if bf16 else "attn_f32_kernel",
             "kernel_ms": round(attn_avg, 5),
             "hbm_gbs_algorithmic": round(abytes / (attn_avg * 1e-3) / 1e9, 1),
         },

@@ -137,14 +137,16 @@ class Case:
         pairs = int(np.sum(n * L + n * (n + 1) // 2))
         return 4 * self.head_dim * self.num_q_heads * pairs
 
-    def algorithmic_bytes(self, append: bool = True) -> int:
-        """K/V read once, Q read, O written, chunk K/V appended."""
+    def algorithmic_bytes(self, append: bool = True, kv_bytes: Optional[int] = None) -> int:
+        """K/V read once, Q read, O written, chunk K/V appended (K/V elements
+        of ``kv_bytes`` each, default the input type's)."""
         e, d, hq, hkv = self.elem_bytes, self.head_dim, self.num_q_heads, self.num_kv_heads
+        ekv = e if kv_bytes is None else kv_bytes
         n = self.seqlen_q.astype(np.int64)
         L = self.cache_len.astype(np.int64)
-        kv = int(np.sum(2 * hkv * d * e * (L + n)))
+        kv = int(np.sum(2 * hkv * d * ekv * (L + n)))
         qo = int(np.sum(2 * hq * d * e * n))
-        ap = int(np.sum(2 * hkv * d * e * n)) if append else 0
+        ap = int(np.sum(2 * hkv * d * ekv * n)) if append else 0
         return kv + qo + ap
 
 
