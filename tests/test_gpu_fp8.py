@@ -85,6 +85,8 @@ SMALL = [
     ("page4", dict(num_q_heads=8, num_kv_heads=1, cache_len=[777], seqlen_q=[100], page_size=4, scale=0.5)),
     ("prefill_L0", dict(num_q_heads=16, num_kv_heads=4, cache_len=[0], seqlen_q=[300], page_size=16, scale=0.5)),
     ("decode_n1", dict(num_q_heads=16, num_kv_heads=1, cache_len=[5000], seqlen_q=[1], page_size=16, scale=0.5)),
+    ("page1024", dict(num_q_heads=16, num_kv_heads=2, cache_len=[2500, 900], seqlen_q=[30, 64], page_size=1024,
+                      scale=0.5, interleave=True)),
 ]
 
 

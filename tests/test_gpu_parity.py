@@ -50,6 +50,11 @@ SMALL = [
                          seqlen_q=[17, 1, 200, 64], page_size=16, scale=0.5, interleave=True)),
     ("f32_ragged", dict(dtype=dg.F32, num_q_heads=4, num_kv_heads=1, head_dim=64, cache_len=[31, 0, 200],
                         seqlen_q=[5, 40, 1], page_size=16, interleave=True)),
+    # pages larger than a 64-key tile: the tile's offset inside the page is a separate term
+    ("bf16_page128", dict(dtype=dg.BF16, num_q_heads=16, num_kv_heads=2, head_dim=128, cache_len=[1000, 130],
+                          seqlen_q=[50, 77], page_size=128, scale=0.5, interleave=True)),
+    ("bf16_page1024_max", dict(dtype=dg.BF16, num_q_heads=8, num_kv_heads=1, head_dim=64, cache_len=[3000],
+                               seqlen_q=[41], page_size=1024, scale=0.5)),
 ]
 
 
