@@ -141,7 +141,8 @@ csr::RopeArgs rope_args(const csr_attn_desc* d, int batch, const void* q, const 
 // integers and the device's CU count, so the size query and the call agree.
 struct Plan {
   int bm, mtiles, nsplit, n_units, xcd_remap;
-  size_t ws_o, ws_lse, ws_bytes;
+  int order_slots;  // > 0: a device-side longest-first order (ragged batches)
+  size_t ws_o, ws_lse, ws_order_off, ws_bytes;
 };
 
 int device_cus() {
@@ -190,6 +191,19 @@ csr_status make_plan(const csr_attn_desc* d, int batch, int total_q, int max_q, 
     p.ws_bytes = ((p.ws_o + 255) & ~(size_t)255) + p.ws_lse;
   } else {
     p.ws_o = p.ws_lse = p.ws_bytes = 0;
+  }
+  // Ragged batches: units differ in length by up to the ratio of the longest
+  // to the shortest sequence, so a device-side plan orders them longest first
+  // per XCD.  Slots per XCD: an eighth of all units plus one whole group, so
+  // the plan's greedy assignment always finds an XCD with room.
+  p.order_slots = 0;
+  p.ws_order_off = 0;
+  const char* ord = getenv("CSR_ORDER");  // 0: keep the fixed order (A/B)
+  const bool want_order = !(ord && atoi(ord) == 0);
+  if (want_order && batch > 1 && (int64_t)batch * d->num_kv_heads <= 1024) {
+    p.order_slots = (int)((units + 7) / 8 + (int64_t)p.mtiles * nsplit);
+    p.ws_order_off = align256(p.ws_bytes);
+    p.ws_bytes = p.ws_order_off + (size_t)8 * p.order_slots * sizeof(int32_t);
   }
   return CSR_OK;
 }
@@ -299,6 +313,25 @@ csr_status run_attention(const csr_attn_desc* d, int batch, const void* q, const
   a.nsplit = p.nsplit;
   a.n_units = p.n_units;
   a.xcd_remap = p.xcd_remap;
+  a.order = nullptr;
+  a.order_slots = 0;
+  if (p.order_slots > 0) {
+    csr::PlanArgs pa;
+    pa.cu_q = cu;
+    pa.cache_len = cache_len;
+    pa.order = reinterpret_cast<int32_t*>(static_cast<char*>(ws) + p.ws_order_off);
+    pa.batch = batch;
+    pa.Hkv = d->num_kv_heads;
+    pa.G = G;
+    pa.bm = p.bm;
+    pa.mtiles = p.mtiles;
+    pa.nsplit = p.nsplit;
+    pa.slots = p.order_slots;
+    st = launched(csr::launch_plan(pa, stream), "work order");
+    if (st != CSR_OK) return st;
+    a.order = pa.order;
+    a.order_slots = p.order_slots;
+  }
   if (g_ev_begin && hipEventRecord(g_ev_begin, stream) != hipSuccess)
     return fail(CSR_E_HIP, "hipEventRecord(begin) failed");
   st = launched(csr::launch_attention(a, d->dtype == CSR_BF16, stream), "attention");

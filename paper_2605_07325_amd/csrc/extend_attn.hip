@@ -136,7 +136,10 @@ template <int BM>
 __device__ __forceinline__ bool decode_unit(const AttnArgs& a, Unit& u) {
   const int w = blockIdx.x;
   int r = w;
-  if (a.xcd_remap) {
+  if (a.order) {
+    r = a.order[w];  // planned on the device (ragged batches): -1 = no unit
+    if (r < 0) return false;
+  } else if (a.xcd_remap) {
     const int q8 = gridDim.x >> 3;  // grid is padded to a multiple of 8
     r = (w & 7) * q8 + (w >> 3);
   }
@@ -907,7 +910,8 @@ int attn_block_m(int dtype_bf16, int d) {
 hipError_t launch_attention(const AttnArgs& a, int dtype_bf16, hipStream_t stream) {
   if (a.n_units == 0) return hipSuccess;
   unsigned grid = (unsigned)a.n_units;
-  if (a.xcd_remap) grid = (grid + 7u) & ~7u;
+  if (a.order) grid = 8u * (unsigned)a.order_slots;
+  else if (a.xcd_remap) grid = (grid + 7u) & ~7u;
   if (dtype_bf16 && a.kv_fp8) {
     // fp8 rows: 8 keys per DMA block
     if (a.P >= 8) hipLaunchKernelGGL((attn_bf16_kernel<128, true, true>), dim3(grid), dim3(512), 0, stream, a);

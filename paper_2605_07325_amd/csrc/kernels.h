@@ -32,11 +32,23 @@ struct AttnArgs {
   int32_t nsplit;            // key-range splits per tile
   int32_t n_units;           // batch * Hkv * nsplit * mtiles
   int32_t xcd_remap;         // 1: keep units that share K/V on one XCD
+  const int32_t* order;      // unit of each workgroup (-1: none), or nullptr for the fixed order
+  int32_t order_slots;       // with `order`: the grid is 8 * order_slots workgroups
 };
 
 // Packed rows (query token x head-in-group) per workgroup for each kernel.
 int attn_block_m(int dtype_bf16, int d);
 hipError_t launch_attention(const AttnArgs& a, int dtype_bf16, hipStream_t stream);
+
+// Longest-first work order for ragged batches (see plan.hip).
+struct PlanArgs {
+  const int32_t* cu_q;
+  const int32_t* cache_len;  // nullptr: every L_b = 0
+  int32_t* order;            // [8 * slots]
+  int32_t batch, Hkv, G, bm, mtiles, nsplit, slots;
+};
+int plan_smem_bytes(int batch, int Hkv);
+hipError_t launch_plan(const PlanArgs& p, hipStream_t stream);
 
 struct MergeArgs {
   const float* part_o;
