@@ -141,6 +141,7 @@ csr::RopeArgs rope_args(const csr_attn_desc* d, int batch, const void* q, const 
 // integers and the device's CU count, so the size query and the call agree.
 struct Plan {
   int bm, mtiles, nsplit, n_units, xcd_remap;
+  int four_waves;   // fp8 cache, at most 128 packed rows per sequence: 4-wave workgroups
   int order_slots;  // > 0: a device-side longest-first order (ragged batches)
   size_t ws_o, ws_lse, ws_order_off, ws_bytes;
 };
@@ -157,7 +158,10 @@ int device_cus() {
 
 csr_status make_plan(const csr_attn_desc* d, int batch, int total_q, int max_q, int max_L, Plan& p) {
   const int G = d->num_q_heads / d->num_kv_heads;
-  p.bm = csr::attn_block_m(d->dtype == CSR_BF16, d->head_dim);
+  // Short chunks over an fp8 cache (decode): one 128-row tile holds every
+  // row of a sequence, and 4-wave workgroups (64 KB of LDS) run two per CU.
+  p.four_waves = kv_fp8(d) && (int64_t)max_q * G <= 128 ? 1 : 0;
+  p.bm = csr::attn_block_m(d->dtype == CSR_BF16, d->head_dim, p.four_waves);
   const int64_t rows = (int64_t)max_q * G;
   if (rows >= (1ll << 30) || (int64_t)max_L + max_q >= (1ll << 30))
     return fail(CSR_E_UNSUPPORTED, "sequence too long (max_seqlen_q*G=%lld, max_cache_len+max_seqlen_q=%lld)",
@@ -170,7 +174,7 @@ csr_status make_plan(const csr_attn_desc* d, int batch, int total_q, int max_q, 
   if (env && atoi(env) > 0) {
     nsplit = atoi(env);
   } else {
-    const int cus = device_cus();
+    const int cus = device_cus() * (p.four_waves ? 2 : 1);  // resident workgroups
     if (base > 0 && base < cus) {
       nsplit = (int)((cus + base - 1) / base);
       const int cap = ntiles / 8 > 1 ? ntiles / 8 : 1;  // keep >= 8 key tiles per split
@@ -307,6 +311,7 @@ csr_status run_attention(const csr_attn_desc* d, int batch, const void* q, const
   a.scale_log2 = scale * 1.4426950408889634f * (kv_fp8(d) ? d->k_scale : 1.f);
   a.v_scale = kv_fp8(d) ? d->v_scale : 1.f;
   a.kv_fp8 = kv_fp8(d) ? 1 : 0;
+  a.four_waves = p.four_waves;
   a.batch = batch;
   a.total_q = total_q;
   a.mtiles = p.mtiles;

@@ -247,11 +247,14 @@ struct TileLoader {
 // Online softmax keeps a per-row reference max and rescales O only when a new
 // score exceeds it by more than 2^8 (wave-uniform branch); probabilities stay
 // below 2^8 and the final normalisation is exact whatever reference was used.
-template <int D, bool SCALAR_PAGES, bool KV8 = false>
-__global__ void __launch_bounds__(512, 1) attn_bf16_kernel(const AttnArgs a) {
+// NW waves per workgroup, 2 waves per SIMD either way: 8 (one workgroup per
+// CU) or, for an fp8 cache whose 64 KB of rings let two workgroups share a
+// CU, 4 -- decode steps then run two computing waves per CU instead of one.
+template <int D, bool SCALAR_PAGES, bool KV8 = false, int NW = 8>
+__global__ void __launch_bounds__(NW * 64, 8 / NW) attn_bf16_kernel(const AttnArgs a) {
   static_assert(!KV8 || D == 128, "fp8 K/V rows are laid out for d = 128");
+  static_assert(NW == 8 || (NW == 4 && KV8), "4-wave workgroups only with the 64 KB fp8 rings");
   typedef typename KFragT<KV8>::type KF;  // one K fragment as read from LDS
-  constexpr int NW = 8;
   constexpr int BM = NW * 32;
   constexpr int ROWB = D * (KV8 ? 1 : 2);  // bytes per key row (bf16 or e4m3 codes)
   constexpr int NCH = ROWB / 16;
@@ -902,8 +905,9 @@ constexpr int BF16_BM = 256;  // 8 waves x 32 packed rows
 
 }  // namespace
 
-int attn_block_m(int dtype_bf16, int d) {
+int attn_block_m(int dtype_bf16, int d, int four_waves) {
   (void)d;
+  if (four_waves) return 128;
   return dtype_bf16 ? BF16_BM : NWAVES * 32;
 }
 
@@ -912,7 +916,11 @@ hipError_t launch_attention(const AttnArgs& a, int dtype_bf16, hipStream_t strea
   unsigned grid = (unsigned)a.n_units;
   if (a.order) grid = 8u * (unsigned)a.order_slots;
   else if (a.xcd_remap) grid = (grid + 7u) & ~7u;
-  if (dtype_bf16 && a.kv_fp8) {
+  if (dtype_bf16 && a.kv_fp8 && a.four_waves) {
+    // fp8 rows, 4 waves: still 8 keys per 1 KB DMA block
+    if (a.P >= 8) hipLaunchKernelGGL((attn_bf16_kernel<128, true, true, 4>), dim3(grid), dim3(256), 0, stream, a);
+    else hipLaunchKernelGGL((attn_bf16_kernel<128, false, true, 4>), dim3(grid), dim3(256), 0, stream, a);
+  } else if (dtype_bf16 && a.kv_fp8) {
     // fp8 rows: 8 keys per DMA block
     if (a.P >= 8) hipLaunchKernelGGL((attn_bf16_kernel<128, true, true>), dim3(grid), dim3(512), 0, stream, a);
     else hipLaunchKernelGGL((attn_bf16_kernel<128, false, true>), dim3(grid), dim3(512), 0, stream, a);

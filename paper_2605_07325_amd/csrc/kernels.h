@@ -27,6 +27,7 @@ struct AttnArgs {
   float scale_log2;          // softmax scale * log2(e) (times k_scale for an fp8 cache)
   float v_scale;             // output multiplier: 1, or v_scale for an fp8 cache
   int32_t kv_fp8;            // K/V (pool and chunk) are OCP e4m3 codes (bf16 q, d = 128)
+  int32_t four_waves;        // fp8 only: 4-wave workgroups of 128 rows, two per CU
   int32_t batch, total_q;
   int32_t mtiles;            // packed-row tiles per (sequence, kv head)
   int32_t nsplit;            // key-range splits per tile
@@ -37,7 +38,7 @@ struct AttnArgs {
 };
 
 // Packed rows (query token x head-in-group) per workgroup for each kernel.
-int attn_block_m(int dtype_bf16, int d);
+int attn_block_m(int dtype_bf16, int d, int four_waves);
 hipError_t launch_attention(const AttnArgs& a, int dtype_bf16, hipStream_t stream);
 
 // Longest-first work order for ragged batches (see plan.hip).

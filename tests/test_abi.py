@@ -194,7 +194,14 @@ def test_fp8_cache_workspace_holds_quantised_chunk():
     both = good_desc(num_q_heads=64, num_kv_heads=4, kv_dtype=csr.CSR_KV_FP8_E4M3, k_scale=0.05, v_scale=0.05,
                      rope_style=csr.CSR_ROPE_NEOX, rope_theta=1e6)
     align = lambda x: (x + 255) // 256 * 256  # noqa: E731
-    for T, L in ((512, 122880), (1, 122880), (7, 0)):
+    # split partials (fp32 O and LSE per split); with no device the plan assumes 256 CUs
+    partials = lambda T, ns: align(ns * T * 64 * 128 * 4) + ns * T * 64 * 4 if ns > 1 else 0  # noqa: E731
+    # (T, L, key splits over a bf16 cache, over an fp8 cache): a decode step over
+    # an fp8 cache runs 4-wave workgroups, two per CU, and doubles its splits
+    for T, L, ns, ns8 in ((512, 122880, 2, 2), (1, 122880, 64, 128), (7, 0, 1, 1)):
         base = csr.extend_workspace_size(plain, 1, T, T, L)
-        assert csr.extend_workspace_size(fp8, 1, T, T, L) - base == 2 * align(T * 4 * 128)
-        assert csr.extend_workspace_size(both, 1, T, T, L) - base == align(T * 64 * 128 * 2) + 2 * align(T * 4 * 128)
+        assert base == partials(T, ns)
+        extra = partials(T, ns8) - partials(T, ns)
+        assert csr.extend_workspace_size(fp8, 1, T, T, L) - base == extra + 2 * align(T * 4 * 128)
+        assert (csr.extend_workspace_size(both, 1, T, T, L) - base
+                == extra + align(T * 64 * 128 * 2) + 2 * align(T * 4 * 128))

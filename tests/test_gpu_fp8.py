@@ -87,6 +87,11 @@ SMALL = [
     ("decode_n1", dict(num_q_heads=16, num_kv_heads=1, cache_len=[5000], seqlen_q=[1], page_size=16, scale=0.5)),
     ("page1024", dict(num_q_heads=16, num_kv_heads=2, cache_len=[2500, 900], seqlen_q=[30, 64], page_size=1024,
                       scale=0.5, interleave=True)),
+    # at most 128 packed rows per sequence: the 4-wave workgroups
+    ("decode_ragged", dict(num_q_heads=32, num_kv_heads=4, cache_len=[0, 1, 4097, 300, 65], seqlen_q=[16, 1, 3, 0, 7],
+                           page_size=16, scale=0.5, interleave=True)),
+    ("decode_page4", dict(num_q_heads=16, num_kv_heads=2, cache_len=[777, 64], seqlen_q=[2, 8], page_size=4,
+                          scale=0.5)),
 ]
 
 
