@@ -142,6 +142,7 @@ csr::RopeArgs rope_args(const csr_attn_desc* d, int batch, const void* q, const 
 struct Plan {
   int bm, mtiles, nsplit, n_units, xcd_remap;
   int four_waves;   // fp8 cache, at most 128 packed rows per sequence: 4-wave workgroups
+  int dma_upper;    // bf16 Q, rows of every unit in the lower half of the waves: the upper half loads K/V
   int order_slots;  // > 0: a device-side longest-first order (ragged batches)
   size_t ws_o, ws_lse, ws_order_off, ws_bytes;
 };
@@ -167,6 +168,10 @@ csr_status make_plan(const csr_attn_desc* d, int batch, int total_q, int max_q, 
     return fail(CSR_E_UNSUPPORTED, "sequence too long (max_seqlen_q*G=%lld, max_cache_len+max_seqlen_q=%lld)",
                 (long long)rows, (long long)max_L + max_q);
   p.mtiles = (int)((rows + p.bm - 1) / p.bm);
+  // Short chunks leave the upper half of the waves without rows: they then
+  // issue all of the K/V DMA, off the computing waves' critical path.
+  const char* dup = getenv("CSR_DMA_UPPER");  // 0: every wave loads (A/B)
+  p.dma_upper = d->dtype == CSR_BF16 && rows <= p.bm / 2 && !(dup && atoi(dup) == 0) ? 1 : 0;
   const int64_t base = (int64_t)batch * d->num_kv_heads * p.mtiles;
   const int ntiles = (max_L + max_q + 63) / 64;
   int nsplit = 1;
@@ -284,7 +289,7 @@ csr_status run_attention(const csr_attn_desc* d, int batch, const void* q, const
   }
   const int G = d->num_q_heads / d->num_kv_heads;
   const float scale = d->softmax_scale > 0.f ? d->softmax_scale : 1.f / sqrtf((float)d->head_dim);
-  csr::AttnArgs a;
+  csr::AttnArgs a{};
   a.q = q;
   a.k_new = k_new;
   a.v_new = v_new;
@@ -312,6 +317,7 @@ csr_status run_attention(const csr_attn_desc* d, int batch, const void* q, const
   a.v_scale = kv_fp8(d) ? d->v_scale : 1.f;
   a.kv_fp8 = kv_fp8(d) ? 1 : 0;
   a.four_waves = p.four_waves;
+  a.dma_upper = p.dma_upper;
   a.batch = batch;
   a.total_q = total_q;
   a.mtiles = p.mtiles;

@@ -250,7 +250,12 @@ struct TileLoader {
 // NW waves per workgroup, 2 waves per SIMD either way: 8 (one workgroup per
 // CU) or, for an fp8 cache whose 64 KB of rings let two workgroups share a
 // CU, 4 -- decode steps then run two computing waves per CU instead of one.
-template <int D, bool SCALAR_PAGES, bool KV8 = false, int NW = 8>
+//
+// DMA_UPPER (short chunks: every packed row of a unit falls in the lower
+// half of the waves): the upper half, which has no rows, issues all of the
+// K/V DMA and the computing waves none, so the DMA issue stalls stay off the
+// computing waves' per-tile dependency chain.
+template <int D, bool SCALAR_PAGES, bool KV8 = false, int NW = 8, bool DMA_UPPER = false>
 __global__ void __launch_bounds__(NW * 64, 8 / NW) attn_bf16_kernel(const AttnArgs a) {
   static_assert(!KV8 || D == 128, "fp8 K/V rows are laid out for d = 128");
   static_assert(NW == 8 || (NW == 4 && KV8), "4-wave workgroups only with the 64 KB fp8 rings");
@@ -262,8 +267,10 @@ __global__ void __launch_bounds__(NW * 64, 8 / NW) attn_bf16_kernel(const AttnAr
   constexpr int DB = D / 32;  // 32-wide d blocks of the output
   constexpr int TILEB = KT * ROWB;
   constexpr int ROWS_PER_KB = 1024 / ROWB;
-  constexpr int NDMA = TILEB / (NW * 1024);  // DMA instructions per wave per tensor tile
+  constexpr int DW = DMA_UPPER ? NW / 2 : NW;  // waves that issue the K/V DMA
+  constexpr int NDMA = TILEB / (DW * 1024);    // DMA instructions per issuing wave per tensor tile
   static_assert(NDMA >= 1, "a tile must give every wave at least one DMA block");
+  constexpr int NH = (NDMA + 1) / 2;           // blocks issued in a tile's first step
   constexpr int ST = 4;                      // ring stages (K and V each)
   constexpr float THRESH = 8.f;              // lazy-rescale threshold (log2 units)
   __shared__ __attribute__((aligned(1024))) char lds[2 * ST * TILEB];
@@ -272,6 +279,10 @@ __global__ void __launch_bounds__(NW * 64, 8 / NW) attn_bf16_kernel(const AttnAr
   if (!decode_unit<BM>(a, u)) return;
 
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  // DMA slot of this wave (clamped to 0 for the computing waves when only the
+  // upper half loads, so that their unused addresses stay in range too)
+  const bool dma_wave = !DMA_UPPER || wave >= NW / 2;
+  const int dw = DMA_UPPER ? max(wave - NW / 2, 0) : wave;
   const int lane = threadIdx.x & 63;
   const int l32 = lane & 31;
   const int h = lane >> 5;
@@ -298,7 +309,7 @@ __global__ void __launch_bounds__(NW * 64, 8 / NW) attn_bf16_kernel(const AttnAr
   // A wave whose 32 rows are all padding (short chunks: n*G < BM) skips the
   // products and exponentials but still issues its share of every K/V DMA
   // and joins every barrier.
-  const bool wave_active = u.m0 + wave * 32 < u.rows_total;
+  const bool wave_active = (!DMA_UPPER || wave < NW / 2) && u.m0 + wave * 32 < u.rows_total;
   const int tok = m_row / G;
   const int lim = u.L + tok;  // last key this lane's row sees
   {
@@ -320,7 +331,7 @@ __global__ void __launch_bounds__(NW * 64, 8 / NW) attn_bf16_kernel(const AttnAr
   const int in_page_mask = min((1 << a.log2P) - 1, KT - 1);
 #pragma unroll
   for (int j = 0; j < NDMA; ++j) {
-    drow[j] = (j * NW + wave) * ROWS_PER_KB + lane / NCH;
+    drow[j] = (j * DW + dw) * ROWS_PER_KB + lane / NCH;
     dchunk[j] = u.g * ROWB + (chunk_of_slot<NCH, KV8>(drow[j], lane % NCH) << 4);
     pool_off[j] = (drow[j] & in_page_mask) * (a.Hkv * ROWB) + dchunk[j];
     new_off[j] = drow[j] * (a.Hkv * ROWB) + dchunk[j];
@@ -332,7 +343,7 @@ __global__ void __launch_bounds__(NW * 64, 8 / NW) attn_bf16_kernel(const AttnAr
   const int64_t page_bytes = (int64_t)kv_stride << log2P;
   auto block_key = [&](int tile, int j) -> int {
     if constexpr (SCALAR_PAGES)
-      return min(tile * KT + (j * NW + wave) * ROWS_PER_KB, last_key);
+      return min(tile * KT + (j * DW + dw) * ROWS_PER_KB, last_key);
     else
       return min(tile * KT + drow[j], last_key);
   };
@@ -352,7 +363,7 @@ __global__ void __launch_bounds__(NW * 64, 8 / NW) attn_bf16_kernel(const AttnAr
   auto page_of = [&](int tile, int j) -> int64_t { return page_off(tile, j, page_id(tile, j)); };
   auto dma = [&](const char* src, char* dst, int j) {
     __builtin_amdgcn_global_load_lds((const __attribute__((address_space(1))) void*)src,
-                                     (__attribute__((address_space(3))) void*)(dst + (j * NW + wave) * 1024), 16, 0, 0);
+                                     (__attribute__((address_space(3))) void*)(dst + (j * DW + dw) * 1024), 16, 0, 0);
   };
   // DMA block j of a K or V tile into `dst`.  A tile wholly inside the prefix
   // or wholly inside the chunk takes a scalar base plus the lane's constant
@@ -383,6 +394,7 @@ __global__ void __launch_bounds__(NW * 64, 8 / NW) attn_bf16_kernel(const AttnAr
     }
   };
   auto issue = [&](int tile, const int64_t* pg, char* dst, const char* pool_base, const char* new_base) {
+    if (!dma_wave) return;
 #pragma unroll
     for (int j = 0; j < NDMA; ++j) issue_block(tile, j, pg[j], dst, pool_base, new_base);
   };
@@ -623,15 +635,17 @@ __global__ void __launch_bounds__(NW * 64, 8 / NW) attn_bf16_kernel(const AttnAr
     int pgi[NDMA];      // their raw page ids, loaded half a tile earlier
     {
       int64_t pg[NDMA];
+      if (dma_wave) {
 #pragma unroll
-      for (int i = 0; i < 3; ++i) {
+        for (int i = 0; i < 3; ++i) {
 #pragma unroll
-        for (int j = 0; j < NDMA; ++j) pg[j] = page_of(clampt(u.tb + i), j);
-        issue(clampt(u.tb + i), pg, kring + i * TILEB, kpool, knew);
-        issue(clampt(u.tb + i), pg, vring + i * TILEB, vpool, vnew);
+          for (int j = 0; j < NDMA; ++j) pg[j] = page_of(clampt(u.tb + i), j);
+          issue(clampt(u.tb + i), pg, kring + i * TILEB, kpool, knew);
+          issue(clampt(u.tb + i), pg, vring + i * TILEB, vpool, vnew);
+        }
       }
 #pragma unroll
-      for (int j = 0; j < NDMA; ++j) pgi[j] = page_id(clampt(u.tb + 3), j);
+      for (int j = 0; j < NDMA; ++j) pgi[j] = dma_wave ? page_id(clampt(u.tb + 3), j) : 0;
     }
     asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
     __syncthreads();
@@ -654,16 +668,32 @@ __global__ void __launch_bounds__(NW * 64, 8 / NW) attn_bf16_kernel(const AttnAr
       // K/V(tb+k+3) replace K/V(tb+k-1), last read during tile k-1; their
       // DMA blocks are spread over the tile's two steps.
       const int nt = clampt(u.tb + k + 3);
+      if (dma_wave) {
 #pragma unroll
-      for (int j = 0; j < NDMA; ++j) pgn[j] = page_off(nt, j, pgi[j]);
+        for (int j = 0; j < NDMA; ++j) pgn[j] = page_off(nt, j, pgi[j]);
+      }
       char* kdst = kring + ((S + 3) % ST) * TILEB;
       char* vdst = vring + ((S + 3) % ST) * TILEB;
       const char* kl = kring + S * TILEB;
-      auto kd0 = [&] { issue_block(nt, 0, pgn[0], kdst, kpool, knew); };
-      auto kd1 = [&] { if constexpr (NDMA > 1) issue_block(nt, NDMA - 1, pgn[NDMA - 1], kdst, kpool, knew); };
-      auto vd0 = [&] { issue_block(nt, 0, pgn[0], vdst, vpool, vnew); };
+      auto kd0 = [&] {
+        if (!dma_wave) return;
+#pragma unroll
+        for (int j = 0; j < NH; ++j) issue_block(nt, j, pgn[j], kdst, kpool, knew);
+      };
+      auto kd1 = [&] {
+        if (!dma_wave) return;
+#pragma unroll
+        for (int j = NH; j < NDMA; ++j) issue_block(nt, j, pgn[j], kdst, kpool, knew);
+      };
+      auto vd0 = [&] {
+        if (!dma_wave) return;
+#pragma unroll
+        for (int j = 0; j < NH; ++j) issue_block(nt, j, pgn[j], vdst, vpool, vnew);
+      };
       auto vd1 = [&] {
-        if constexpr (NDMA > 1) issue_block(nt, NDMA - 1, pgn[NDMA - 1], vdst, vpool, vnew);
+        if (!dma_wave) return;
+#pragma unroll
+        for (int j = NH; j < NDMA; ++j) issue_block(nt, j, pgn[j], vdst, vpool, vnew);
 #pragma unroll
         for (int j = 0; j < NDMA; ++j) pgi[j] = page_id(clampt(u.tb + k + 4), j);
       };
@@ -698,7 +728,7 @@ __global__ void __launch_bounds__(NW * 64, 8 / NW) attn_bf16_kernel(const AttnAr
   for (int it = max(main_end, u.tb); it < u.te; ++it) {
     int64_t pg[NDMA];
 #pragma unroll
-    for (int j = 0; j < NDMA; ++j) pg[j] = page_of(it, j);
+    for (int j = 0; j < NDMA; ++j) pg[j] = dma_wave ? page_of(it, j) : 0;
     issue(it, pg, kring, kpool, knew);
     issue(it, pg, vring, vpool, vnew);
     asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
@@ -911,6 +941,19 @@ int attn_block_m(int dtype_bf16, int d, int four_waves) {
   return dtype_bf16 ? BF16_BM : NWAVES * 32;
 }
 
+namespace {
+
+// One bf16-Q kernel variant, with the DMA issued by every wave or by the upper half only.
+template <int D, bool SCALAR_PAGES, bool KV8, int NW>
+void launch_bf16(const AttnArgs& a, unsigned grid, hipStream_t stream) {
+  if (a.dma_upper)
+    hipLaunchKernelGGL((attn_bf16_kernel<D, SCALAR_PAGES, KV8, NW, true>), dim3(grid), dim3(NW * 64), 0, stream, a);
+  else
+    hipLaunchKernelGGL((attn_bf16_kernel<D, SCALAR_PAGES, KV8, NW, false>), dim3(grid), dim3(NW * 64), 0, stream, a);
+}
+
+}  // namespace
+
 hipError_t launch_attention(const AttnArgs& a, int dtype_bf16, hipStream_t stream) {
   if (a.n_units == 0) return hipSuccess;
   unsigned grid = (unsigned)a.n_units;
@@ -918,21 +961,21 @@ hipError_t launch_attention(const AttnArgs& a, int dtype_bf16, hipStream_t strea
   else if (a.xcd_remap) grid = (grid + 7u) & ~7u;
   if (dtype_bf16 && a.kv_fp8 && a.four_waves) {
     // fp8 rows, 4 waves: still 8 keys per 1 KB DMA block
-    if (a.P >= 8) hipLaunchKernelGGL((attn_bf16_kernel<128, true, true, 4>), dim3(grid), dim3(256), 0, stream, a);
-    else hipLaunchKernelGGL((attn_bf16_kernel<128, false, true, 4>), dim3(grid), dim3(256), 0, stream, a);
+    if (a.P >= 8) launch_bf16<128, true, true, 4>(a, grid, stream);
+    else launch_bf16<128, false, true, 4>(a, grid, stream);
   } else if (dtype_bf16 && a.kv_fp8) {
-    // fp8 rows: 8 keys per DMA block
+    // fp8 rows: 8 keys per DMA block (more than 128 packed rows: every wave computes)
     if (a.P >= 8) hipLaunchKernelGGL((attn_bf16_kernel<128, true, true>), dim3(grid), dim3(512), 0, stream, a);
     else hipLaunchKernelGGL((attn_bf16_kernel<128, false, true>), dim3(grid), dim3(512), 0, stream, a);
   } else if (dtype_bf16) {
     // Scalar page-id loads need every DMA block (4 keys at d=128, 8 at d=64) inside one page.
     const bool scalar_pages = a.P >= (a.d == 128 ? 4 : 8);
     if (a.d == 128) {
-      if (scalar_pages) hipLaunchKernelGGL((attn_bf16_kernel<128, true>), dim3(grid), dim3(512), 0, stream, a);
-      else hipLaunchKernelGGL((attn_bf16_kernel<128, false>), dim3(grid), dim3(512), 0, stream, a);
+      if (scalar_pages) launch_bf16<128, true, false, 8>(a, grid, stream);
+      else launch_bf16<128, false, false, 8>(a, grid, stream);
     } else {
-      if (scalar_pages) hipLaunchKernelGGL((attn_bf16_kernel<64, true>), dim3(grid), dim3(512), 0, stream, a);
-      else hipLaunchKernelGGL((attn_bf16_kernel<64, false>), dim3(grid), dim3(512), 0, stream, a);
+      if (scalar_pages) launch_bf16<64, true, false, 8>(a, grid, stream);
+      else launch_bf16<64, false, false, 8>(a, grid, stream);
     }
   } else {
     if (a.d == 128) hipLaunchKernelGGL((attn_f32_kernel<128>), dim3(grid), dim3(NTHREADS), 0, stream, a);

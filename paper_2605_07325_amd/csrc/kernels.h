@@ -28,6 +28,7 @@ struct AttnArgs {
   float v_scale;             // output multiplier: 1, or v_scale for an fp8 cache
   int32_t kv_fp8;            // K/V (pool and chunk) are OCP e4m3 codes (bf16 q, d = 128)
   int32_t four_waves;        // fp8 only: 4-wave workgroups of 128 rows, two per CU
+  int32_t dma_upper;         // bf16 Q: all rows in the lower half of the waves; the upper half loads K/V
   int32_t batch, total_q;
   int32_t mtiles;            // packed-row tiles per (sequence, kv head)
   int32_t nsplit;            // key-range splits per tile

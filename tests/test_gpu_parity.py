@@ -174,6 +174,24 @@ def test_short_chunks_all_rows(label, kw, nsplit):
     np.testing.assert_array_equal(from_dev(case, dev.v_pool), vp)
 
 
+@pytest.mark.parametrize("label,kw", DECODE, ids=[d[0] for d in DECODE])
+def test_short_chunks_dma_issuers_do_not_change_results(label, kw):
+    """Short chunks load K/V from the waves without rows; the loads land in the
+    same places as when every wave loads, so the outputs are identical bits."""
+    case = dg.make_case(label, seed=2, cfg_id=311, **kw)
+    note(f"{label}: K/V loads from the upper waves vs from every wave")
+    outs = []
+    for flag in ("1", "0"):
+        os.environ["CSR_DMA_UPPER"] = flag
+        try:
+            out, lse = Dev(case).extend()
+            torch.cuda.synchronize()
+        finally:
+            os.environ.pop("CSR_DMA_UPPER", None)
+        outs.append((out.view(torch.int16).cpu(), lse.cpu()))
+    assert torch.equal(outs[0][0], outs[1][0]) and torch.equal(outs[0][1], outs[1][1])
+
+
 @pytest.mark.parametrize("n", [1, 8])
 def test_c3_decode_120k_prefix_all_rows(n):
     case = dg.config(f"c3_{n}")
