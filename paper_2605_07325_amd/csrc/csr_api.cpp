@@ -277,7 +277,8 @@ csr::AppendArgs append_args(const csr_attn_desc* d, int batch, const void* k_new
 csr_status run_attention(const csr_attn_desc* d, int batch, const void* q, const void* k_new, const void* v_new,
                          const void* k_pool, const void* v_pool, int num_pages, const int32_t* bt, int bt_stride,
                          const int32_t* cu, const int32_t* cache_len, int total_q, int max_q, int max_L, void* out,
-                         float* lse, void* ws, size_t ws_bytes, hipStream_t stream) {
+                         float* lse, void* ws, size_t ws_bytes, hipStream_t stream,
+                         const csr::AppendArgs* app = nullptr) {
   Plan p;
   csr_status st = make_plan(d, batch, total_q, max_q, max_L, p);
   if (st != CSR_OK) return st;
@@ -286,6 +287,13 @@ csr_status run_attention(const csr_attn_desc* d, int batch, const void* q, const
     if (ws_bytes < p.ws_bytes)
       return fail(CSR_E_WORKSPACE, "workspace of %zu bytes required, got %zu", p.ws_bytes, ws_bytes);
     if (!aligned16(ws)) return fail(CSR_E_INVAL, "workspace must be 16-byte aligned");
+  }
+  // The append writes only slots [L_b, L_b + n_b), which this attention
+  // never reads: with a merge launch it rides along in that launch, else it
+  // is a launch of its own.
+  if (app && p.nsplit == 1) {
+    st = launched(csr::launch_append(*app, stream), "kv_append");
+    if (st != CSR_OK) return st;
   }
   const int G = d->num_q_heads / d->num_kv_heads;
   const float scale = d->softmax_scale > 0.f ? d->softmax_scale : 1.f / sqrtf((float)d->head_dim);
@@ -349,7 +357,8 @@ csr_status run_attention(const csr_attn_desc* d, int batch, const void* q, const
   if (st != CSR_OK) return st;
   if (g_ev_end && hipEventRecord(g_ev_end, stream) != hipSuccess) return fail(CSR_E_HIP, "hipEventRecord(end) failed");
   if (p.nsplit == 1) return st;
-  csr::MergeArgs m;
+  csr::MergeArgs m{};
+  if (app) m.append = *app;
   m.part_o = a.part_o;
   m.part_lse = a.part_lse;
   m.out = out;
@@ -477,15 +486,11 @@ csr_status csr_extend_attention(const csr_attn_desc* desc, int32_t batch, const 
                          max_cache_len > 0 ? cache_seqlens : nullptr, total_q, max_seqlen_q, max_cache_len, out, lse,
                          p.ws_bytes ? ws + pl.bytes : nullptr, workspace_bytes - pl.bytes, s);
   }
-  if (append) {
-    const csr::AppendArgs a = append_args(desc, batch, k_new, v_new, k_pool, v_pool, num_pages, block_table,
+  const csr::AppendArgs app = append_args(desc, batch, k_new, v_new, k_pool, v_pool, num_pages, block_table,
                                           bt_stride, cu_seqlens_q, cache_seqlens, total_q);
-    st = launched(csr::launch_append(a, s), "kv_append");
-    if (st != CSR_OK) return st;
-  }
   return run_attention(desc, batch, q, k_new, v_new, k_pool, v_pool, num_pages, block_table, bt_stride, cu_seqlens_q,
                        max_cache_len > 0 ? cache_seqlens : nullptr, total_q, max_seqlen_q, max_cache_len, out, lse,
-                       workspace, workspace_bytes, s);
+                       workspace, workspace_bytes, s, append ? &app : nullptr);
 }
 
 csr_status csr_prefill(const csr_attn_desc* desc, int32_t batch, const void* q, const void* k, const void* v,

@@ -52,15 +52,6 @@ struct PlanArgs {
 int plan_smem_bytes(int batch, int Hkv);
 hipError_t launch_plan(const PlanArgs& p, hipStream_t stream);
 
-struct MergeArgs {
-  const float* part_o;
-  const float* part_lse;
-  void* out;
-  float* lse;
-  int32_t nsplit, total_q, Hq, d;
-};
-hipError_t launch_merge(const MergeArgs& a, int dtype_bf16, hipStream_t stream);
-
 struct AppendArgs {
   const void* k_new;
   const void* v_new;
@@ -73,6 +64,19 @@ struct AppendArgs {
   int32_t row_chunks;        // 16-byte chunks per (token, kv head) row = d * elem / 16
 };
 hipError_t launch_append(const AppendArgs& a, hipStream_t stream);
+
+struct MergeArgs {
+  const float* part_o;
+  const float* part_lse;
+  void* out;
+  float* lse;
+  int32_t nsplit, total_q, Hq, d;
+  // An append carried by the same launch (extra workgroups after the merge's;
+  // append.total_q == 0: none).  It writes only cache slots [L_b, L_b + n_b),
+  // which the attention of the same call never reads.
+  AppendArgs append;
+};
+hipError_t launch_merge(const MergeArgs& a, int dtype_bf16, hipStream_t stream);
 
 // Rotary embedding at absolute positions L_b + i and/or fp8 quantisation of
 // K/V, fused with the append.

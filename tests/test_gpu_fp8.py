@@ -92,6 +92,9 @@ SMALL = [
                            page_size=16, scale=0.5, interleave=True)),
     ("decode_page4", dict(num_q_heads=16, num_kv_heads=2, cache_len=[777, 64], seqlen_q=[2, 8], page_size=4,
                           scale=0.5)),
+    # ragged decode batch, pages smaller than a DMA block
+    ("decode_ragged_page4", dict(num_q_heads=16, num_kv_heads=4, cache_len=[5000, 1, 700, 0], seqlen_q=[8, 1, 3, 5],
+                          page_size=4, scale=0.5, interleave=True)),
 ]
 
 

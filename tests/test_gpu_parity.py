@@ -152,6 +152,11 @@ DECODE = [
                                seqlen_q=[2, 16], page_size=4, scale=0.5)),
     ("decode_g2_rows40", dict(dtype=dg.BF16, num_q_heads=8, num_kv_heads=4, head_dim=128, cache_len=[700, 0, 95],
                               seqlen_q=[20, 7, 1], page_size=8, scale=0.5)),
+    # ragged decode batches over small and large pages
+    ("decode_d64_ragged", dict(dtype=dg.BF16, num_q_heads=16, num_kv_heads=2, head_dim=64, cache_len=[3000, 100, 0, 33],
+                              seqlen_q=[1, 8, 3, 2], page_size=4, scale=0.5, interleave=True)),
+    ("decode_n1_batch4", dict(dtype=dg.BF16, num_q_heads=64, num_kv_heads=4, head_dim=128, cache_len=[9000, 64, 65, 1],
+                             seqlen_q=[1, 1, 1, 1], page_size=16, scale=0.5, interleave=True)),
 ]
 
 
