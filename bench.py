@@ -98,6 +98,23 @@ class HipEvents:
         self.hip.hipEventDestroy(ctypes.c_void_p(ev))
 
 
+def measured_mfma_peak(torch):
+    """Dense bf16 MFMA ceiling measured on this device (benchmark-support
+    library: chains of v_mfma_f32_32x32x16_bf16, two waves per SIMD, one
+    workgroup per CU) and the shader clock the loop ran at."""
+    path = os.path.join(os.path.dirname(os.path.abspath(__file__)), "paper_2605_07325_amd", "libcsr_bench.so")
+    lib = ctypes.CDLL(path)
+    fn = lib.csr_bench_mfma_peak
+    fn.restype = ctypes.c_int
+    fn.argtypes = [ctypes.c_int, ctypes.c_int] + [ctypes.POINTER(ctypes.c_double)] * 3
+    wgs = torch.cuda.get_device_properties(0).multi_processor_count
+    ms, fl, ghz = ctypes.c_double(), ctypes.c_double(), ctypes.c_double()
+    rc = fn(wgs, 20000, ctypes.byref(ms), ctypes.byref(fl), ctypes.byref(ghz))
+    if rc != 0:
+        raise RuntimeError(f"csr_bench_mfma_peak failed (HIP error {rc})")
+    return fl.value / 1e12, ghz.value, ms.value
+
+
 def cpu_baseline(case, target_s: float):
     """The fp64 oracle timed on this host's cores on a bounded sample of the
     same workload's query tokens (all heads of each sampled token)."""
@@ -470,6 +487,15 @@ def main():
     plain_ms = hookless_ms(desc)
     rec["ms_per_step_without_event_hook"] = round(plain_ms, 5)
     log(f"same steps without the attention event hook: {plain_ms:.4f} ms/step")
+    if bf16:
+        mtf, mghz, mms = measured_mfma_peak(torch)
+        rec["roofline"]["measured_mfma"] = {
+            "tflops": round(mtf, 1), "clock_ghz": round(mghz, 3), "frac": round(achieved / mtf, 4),
+            "loop": "v_mfma_f32_32x32x16_bf16, 4 chains per wave, 2 waves per SIMD, one workgroup per CU",
+            "loop_ms": round(mms, 3),
+        }
+        log(f"measured MFMA ceiling {mtf:.0f} TFLOP/s at {mghz:.2f} GHz shader clock: the attention kernel "
+            f"reaches {100 * achieved / mtf:.1f}% of it ({100 * achieved / peak:.1f}% of the published peak)")
     if rope_style:
         # Same process, same inputs, both without the hook: the step without the rotation.
         unrotated_ms = hookless_ms(plain_desc)

@@ -1,7 +1,9 @@
 """Build libcsr.so (HIP kernels + C ABI) for gfx950 in-tree with hipcc.
 
 ``python -m paper_2605_07325_amd.build`` compiles every source under ``csrc/``
-into ``paper_2605_07325_amd/libcsr.so``.  It always recompiles.
+into ``paper_2605_07325_amd/libcsr.so``, and the benchmark-support sources under
+``bench_csrc/`` (a measured MFMA ceiling) into ``libcsr_bench.so``.  It always
+recompiles.
 """
 from __future__ import annotations
 
@@ -15,6 +17,8 @@ PKG = os.path.dirname(os.path.abspath(__file__))
 CSRC = os.path.join(PKG, "csrc")
 OBJ = os.path.join(PKG, "_build")
 LIB = os.path.join(PKG, "libcsr.so")
+BENCH_CSRC = os.path.join(PKG, "bench_csrc")
+BENCH_LIB = os.path.join(PKG, "libcsr_bench.so")
 ROOT = os.path.dirname(PKG)
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 ARCH = "gfx950"
@@ -34,11 +38,11 @@ def _compile(src: str, obj_dir: str = OBJ, defines=()) -> str:
     return obj
 
 
-def build(verbose: bool = False, out: str = LIB, defines=()) -> str:
-    """Compile every source and link ``out``; ``defines`` are extra -D macros."""
-    obj_dir = OBJ if out == LIB else out + ".objs"
+def build(verbose: bool = False, out: str = LIB, defines=(), src_dir: str = CSRC) -> str:
+    """Compile every source of ``src_dir`` and link ``out``; ``defines`` are extra -D macros."""
+    obj_dir = OBJ if out == LIB else (os.path.join(OBJ, "bench") if out == BENCH_LIB else out + ".objs")
     os.makedirs(obj_dir, exist_ok=True)
-    srcs = sorted(glob.glob(os.path.join(CSRC, "*.hip")) + glob.glob(os.path.join(CSRC, "*.cpp")))
+    srcs = sorted(glob.glob(os.path.join(src_dir, "*.hip")) + glob.glob(os.path.join(src_dir, "*.cpp")))
     with concurrent.futures.ThreadPoolExecutor(max_workers=min(8, len(srcs))) as ex:
         objs = list(ex.map(lambda s: _compile(s, obj_dir, defines), srcs))
     tmp = out + ".tmp"
@@ -52,6 +56,12 @@ def build(verbose: bool = False, out: str = LIB, defines=()) -> str:
     return out
 
 
+def build_bench(verbose: bool = False) -> str:
+    """Benchmark-support library (not part of the C ABI of libcsr)."""
+    return build(verbose=verbose, out=BENCH_LIB, src_dir=BENCH_CSRC)
+
+
 if __name__ == "__main__":
     build(verbose=True)
+    build_bench(verbose=True)
     sys.exit(0)

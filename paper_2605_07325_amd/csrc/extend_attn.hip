@@ -160,9 +160,11 @@ __device__ __forceinline__ bool decode_unit(const AttnArgs& a, Unit& u) {
   const int m_last = min(u.m0 + BM, u.rows_total) - 1;
   u.kv_end = u.L + m_last / a.G + 1;
   const int ntiles = (u.kv_end + KT - 1) / KT;
-  const int per = (ntiles + a.nsplit - 1) / a.nsplit;
-  u.tb = u.s * per;
-  u.te = min(ntiles, u.tb + per);
+  // Split sizes differ by at most one tile, the larger ones first: the last
+  // split holds the diagonal (masked, unpipelined) tiles and gets the smaller share.
+  const int q = ntiles / a.nsplit, rem = ntiles - q * a.nsplit;
+  u.tb = u.s * q + min(u.s, rem);
+  u.te = u.tb + q + (u.s < rem ? 1 : 0);
   return true;
 }
 

@@ -1,0 +1,41 @@
+"""The benchmark-support library (measured MFMA ceiling quoted by bench.py)."""
+import ctypes
+import os
+
+import pytest
+
+LIB = os.path.join(os.path.dirname(os.path.dirname(os.path.abspath(__file__))), "paper_2605_07325_amd",
+                   "libcsr_bench.so")
+
+
+def _fn():
+    lib = ctypes.CDLL(LIB)
+    fn = lib.csr_bench_mfma_peak
+    fn.restype = ctypes.c_int
+    fn.argtypes = [ctypes.c_int, ctypes.c_int] + [ctypes.POINTER(ctypes.c_double)] * 3
+    return fn
+
+
+def test_loads_and_rejects_bad_arguments_before_any_device_call():
+    fn = _fn()
+    d = [ctypes.c_double() for _ in range(3)]
+    assert fn(0, 100, *map(ctypes.byref, d)) != 0
+    assert fn(4, 0, *map(ctypes.byref, d)) != 0
+
+
+@pytest.mark.gpu
+def test_measured_ceiling_is_plausible():
+    import torch
+
+    torch.cuda.init()
+    fn = _fn()
+    ms, fl, ghz = ctypes.c_double(), ctypes.c_double(), ctypes.c_double()
+    wgs = torch.cuda.get_device_properties(0).multi_processor_count
+    assert fn(wgs, 4000, ctypes.byref(ms), ctypes.byref(fl), ctypes.byref(ghz)) == 0
+    tflops = fl.value / 1e12
+    print(f"measured MFMA ceiling {tflops:.0f} TFLOP/s at {ghz.value:.2f} GHz ({ms.value:.3f} ms)", flush=True)
+    # dense bf16: at most the published 2.5 PFLOP/s (2.4 GHz); the clock is a shader clock in GHz
+    assert 500 < tflops < 2600
+    assert 0.5 < ghz.value < 2.6
+    # the loop issues one 32x32x16 MFMA per 32 clocks per SIMD at most
+    assert tflops <= wgs * 4 * 32768 / 32 * ghz.value * 1e9 / 1e12 * 1.02
