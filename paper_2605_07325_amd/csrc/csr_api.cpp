@@ -203,8 +203,9 @@ csr_status make_plan(const csr_attn_desc* d, int batch, int total_q, int max_q, 
   }
   // Ragged batches: units differ in length by up to the ratio of the longest
   // to the shortest sequence, so a device-side plan orders them longest first
-  // per XCD.  Slots per XCD: an eighth of all units plus one whole group, so
-  // the plan's greedy assignment always finds an XCD with room.
+  // per XCD.  Slots per XCD: an eighth of all units plus one whole group (no
+  // subgroup is larger), so the plan's greedy assignment always finds an XCD
+  // with room.
   p.order_slots = 0;
   p.ws_order_off = 0;
   const char* ord = getenv("CSR_ORDER");  // 0: keep the fixed order (A/B)
@@ -346,6 +347,7 @@ csr_status run_attention(const csr_attn_desc* d, int batch, const void* q, const
     pa.mtiles = p.mtiles;
     pa.nsplit = p.nsplit;
     pa.slots = p.order_slots;
+    pa.rt_per_sub = csr::plan_subgroup_rows(batch, d->num_kv_heads, p.mtiles);
     st = launched(csr::launch_plan(pa, stream), "work order");
     if (st != CSR_OK) return st;
     a.order = pa.order;

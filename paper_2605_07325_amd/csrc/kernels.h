@@ -48,8 +48,10 @@ struct PlanArgs {
   const int32_t* cache_len;  // nullptr: every L_b = 0
   int32_t* order;            // [8 * slots]
   int32_t batch, Hkv, G, bm, mtiles, nsplit, slots;
+  int32_t rt_per_sub;        // row tiles per subgroup (the XCD-assignment granule)
 };
-int plan_smem_bytes(int batch, int Hkv);
+int plan_subgroup_rows(int batch, int Hkv, int mtiles);
+int plan_smem_bytes(int batch, int Hkv, int mtiles, int rt_per_sub);
 hipError_t launch_plan(const PlanArgs& p, hipStream_t stream);
 
 struct AppendArgs {
