@@ -166,9 +166,12 @@ size_t csr_extend_workspace_size(const csr_attn_desc* desc, int32_t batch, int32
  *   max_seqlen_q      host upper bound of n_b; max_cache_len host upper bound
  *                     of L_b (they size the launch; exceeding them is an error
  *                     the library cannot detect)
- *   flags             CSR_APPEND: enqueue csr_kv_append first (the attention
- *                     itself reads chunk keys from k_new / v_new either way,
- *                     or from their rotated workspace copies with RoPE)
+ *   flags             CSR_APPEND: also append the chunk exactly as
+ *                     csr_kv_append does, within this call's stream work
+ *                     (before the attention, or in the split-K merge launch
+ *                     after it: the attention reads chunk keys from k_new /
+ *                     v_new, or from their prepared workspace copies, and
+ *                     never reads the slots being appended)
  *   q, k_new          with desc->rope_style set: unrotated projections; one
  *                     fused launch writes their rotations at L_b + i to the
  *                     workspace (and, with CSR_APPEND, the rotated keys and
