@@ -69,6 +69,15 @@
  * [0, num_pages); ids outside that range are never dereferenced (attention
  * reads some other in-bounds key row in its place, the append row is dropped)
  * so a bad table cannot fault the GPU, but the result is then unspecified.
+ *
+ * Environment overrides (testing and A/B measurement only; read at every
+ * call, so a workspace query and the call it sizes must see the same values):
+ *   CSR_NSPLIT=k      split the key range of every unit into k parts (changes
+ *                     the summation order: results move within rounding)
+ *   CSR_ORDER=0       ragged batches run their units in index order instead of
+ *                     the device-side longest-first order (identical results)
+ *   CSR_DMA_UPPER=0   short chunks load K/V from every wave instead of only the
+ *                     waves without rows (identical results)
  */
 #ifndef CSR_H
 #define CSR_H
