@@ -23,8 +23,9 @@ steps the difference is visible, for the 512-token chunk it is below 1 %.
 inside the step (one fused rotate-and-append launch before the attention) and
 reports the hook-free step time with and without the rotation.
 
-Prints one JSON line.  ``--gpus N`` with N > 1 is rejected: this build runs
-on one GPU.
+Prints one JSON line.  ``--gpus N`` with N > 1 is rejected: the benchmark
+measures one GPU (the attention shards without communication by kv head and
+by sequence; that split is not run here).
 """
 from __future__ import annotations
 
