@@ -6,9 +6,10 @@
 // device-side (cache_seqlens, cu_seqlens_q), so the order is formed on the
 // device, by one workgroup, before the attention launch:
 //  * the row tiles of a group (b, g) share one K/V stream; they are cut into
-//    subgroups of up to K consecutive row tiles, and a subgroup stays on one
-//    XCD (its L2 serves every row tile of the subgroup).  Whole groups would be
-//    too coarse: one long sequence's group can exceed an XCD's fair share;
+//    subgroups of up to K consecutive row tiles (K = 4 unless the batch is
+//    very large), and a subgroup stays on one XCD (its L2 serves every row
+//    tile of the subgroup).  Whole groups would be too coarse: one long
+//    sequence's group can exceed an XCD's fair share;
 //  * subgroups are ranked by per-unit length, longest first, and each goes to
 //    the XCD with the least work so far among those with room left (greedy
 //    longest-processing-time assignment);
@@ -41,6 +42,8 @@ __global__ void __launch_bounds__(kPlanThreads) plan_units_kernel(PlanArgs p) {
   int* by_rank = sgrp + cap;      // subgroup of each rank
   int* sslot = by_rank + cap;     // first slot of the subgroup in its XCD's queue
   int* sxcd = sslot + cap;
+  int* rk_units = sxcd + cap;     // units and per-unit length in rank order
+  int* rk_len = rk_units + cap;
   const int tid = threadIdx.x;
 
   for (int w = tid; w < p.slots * 8; w += kPlanThreads) p.order[w] = -1;
@@ -78,24 +81,42 @@ __global__ void __launch_bounds__(kPlanThreads) plan_units_kernel(PlanArgs p) {
   __syncthreads();
   // Rank: longer first, ties by subgroup index (a permutation of 0 .. nsg-1).
   for (int s = tid; s < nsg; s += kPlanThreads) {
+    const int ls = slen[s];
     int r = 0;
-    for (int j = 0; j < nsg; ++j) r += (slen[j] > slen[s]) || (slen[j] == slen[s] && j < s);
+#pragma unroll 8
+    for (int j = 0; j < nsg; ++j) r += (slen[j] > ls) || (slen[j] == ls && j < s);
     by_rank[r] = s;
+    rk_units[r] = sunits[s];
+    rk_len[r] = ls;
   }
   __syncthreads();
-  if (tid == 0) {
-    long long load[8] = {0, 0, 0, 0, 0, 0, 0, 0};
-    int count[8] = {0, 0, 0, 0, 0, 0, 0, 0};
+  if (tid < 8) {
+    // Greedy assignment, one lane per XCD: lane x holds XCD x's unit count
+    // and work; each subgroup goes to the lane with the least work among
+    // those with room (ties: the lower XCD), found with three xor shuffles
+    // over keys (work << 3 | x).
+    const int x = tid;
+    int count = 0;
+    unsigned long long load = 0;
     for (int r = 0; r < nsg; ++r) {
-      const int s = by_rank[r];
-      int best = -1;
-      for (int x = 0; x < 8; ++x)
-        if (count[x] + sunits[s] <= p.slots && (best < 0 || load[x] < load[best])) best = x;
-      if (best < 0) best = 0;  // unreachable with the host's slot bound; writes below stay in range
-      sxcd[s] = best;
-      sslot[s] = count[best];
-      count[best] += sunits[s];
-      load[best] += (long long)sunits[s] * slen[s];
+      const int su = rk_units[r];
+      const unsigned long long key =
+          count + su <= p.slots ? (load << 3) | (unsigned long long)x : ~0ull;
+      unsigned long long m = key;
+#pragma unroll
+      for (int o = 1; o < 8; o <<= 1) {
+        const unsigned long long other = __shfl_xor(m, o, 8);
+        m = other < m ? other : m;
+      }
+      // (no XCD with room is unreachable with the host's slot bound: XCD 0 then)
+      const int best = m == ~0ull ? 0 : (int)(m & 7);
+      if (x == best) {
+        const int s = by_rank[r];
+        sxcd[s] = best;
+        sslot[s] = count;
+        count += su;
+        load += (unsigned long long)su * (unsigned long long)rk_len[r];
+      }
     }
   }
   __syncthreads();
@@ -119,13 +140,17 @@ __global__ void __launch_bounds__(kPlanThreads) plan_units_kernel(PlanArgs p) {
 }  // namespace
 
 int plan_subgroup_rows(int batch, int Hkv, int mtiles) {
-  // at most ~1024 + batch * Hkv subgroups: the shared arrays stay under 64 KB
-  const int64_t need = ((int64_t)batch * Hkv * mtiles + 1023) / 1024;
-  return (int)(need > 8 ? need : 8);
+  // 4 row tiles (measured on the 8-sequence ragged batch: 4 beat 1, 2, 8, 16
+  // and 32), more when needed to keep at most 768 + batch * Hkv <= 1792
+  // subgroups (the host plans batches of at most 1024 groups): the shared
+  // arrays (8 ints per subgroup) then stay under 64 KB and the ranking's cost,
+  // quadratic in the subgroup count, stays small
+  const int64_t need = ((int64_t)batch * Hkv * mtiles + 767) / 768;
+  return (int)(need > 4 ? need : 4);
 }
 
 int plan_smem_bytes(int batch, int Hkv, int mtiles, int rt_per_sub) {
-  return (batch * Hkv + 1 + 6 * subgroup_cap(batch, Hkv, mtiles, rt_per_sub)) * (int)sizeof(int);
+  return (batch * Hkv + 1 + 8 * subgroup_cap(batch, Hkv, mtiles, rt_per_sub)) * (int)sizeof(int);
 }
 
 hipError_t launch_plan(const PlanArgs& p, hipStream_t stream) {

@@ -68,7 +68,7 @@ def test_work_order_is_a_longest_first_permutation(nsplit):
     got = order[order >= 0]
     assert len(got) == len(set(got.tolist())), "a unit is scheduled twice"
     assert set(got.tolist()) == active, "scheduled units differ from the active units"
-    spread = math.ceil(8 * BM / G / 64 / nsplit) + 1  # key tiles between the row tiles of one subgroup
+    spread = math.ceil(4 * BM / G / 64 / nsplit) + 1  # key tiles between the row tiles of one subgroup
     loads = []
     for x in range(8):
         q = [length(int(u)) for u in order[:, x] if u >= 0]
