@@ -125,12 +125,14 @@ def test_fp8_kv_append_alone():
     check_pool8(case, dev, case.cache_len)
 
 
+@pytest.mark.parametrize("n", [[90], [1, 2, 1]], ids=["chunk90", "decode"])
 @pytest.mark.parametrize("style", [csr.CSR_ROPE_NEOX, csr.CSR_ROPE_INTERLEAVED])
-def test_fp8_with_rope(style):
-    case = fp8_case("rope8", 602, num_q_heads=16, num_kv_heads=2, cache_len=[3000], seqlen_q=[90], page_size=16,
-                    scale=0.5)
+def test_fp8_with_rope(style, n):
+    L = [3000] if len(n) == 1 else [3000, 64, 777]
+    case = fp8_case("rope8", 602, num_q_heads=16, num_kv_heads=2, cache_len=L, seqlen_q=n, page_size=16,
+                    scale=0.5, interleave=len(n) > 1)
     rope = (style, 0, 1e6)
-    note(f"fp8 + rope style {style}: csr_extend_attention(APPEND)")
+    note(f"fp8 + rope style {style}, L={L} n={n}: csr_extend_attention(APPEND)")
     dev = Dev8(case, rope)
     out, lse = dev.extend(append=True)
     torch.cuda.synchronize()
