@@ -214,3 +214,34 @@ def test_no_op_and_error_paths_on_device():
         csr.extend_attention(dev.desc, dev.q, dev.k_new, dev.v_new, dev.k_pool, dev.v_pool, None, case.bt_stride,
                              dev.cu, dev.cache_len, case.max_seqlen_q + 1000, case.max_cache_len)
     assert e.value.status == csr.CSR_E_INVAL
+
+
+def test_out_of_range_page_ids_stay_contained():
+    """Page ids outside [0, num_pages) in one sequence's table are never
+    dereferenced: its attention reads some in-bounds row in their place (its
+    output is unspecified but finite), its appends to such pages are dropped,
+    and every other sequence's output and appended rows are exact."""
+    case = dg.make_case("badpages", dtype=dg.BF16, num_q_heads=16, num_kv_heads=2, head_dim=128, cache_len=[700, 900],
+                        seqlen_q=[20, 33], page_size=16, scale=0.5, seed=8, cfg_id=340, interleave=True)
+    P, npages = case.page_size, case.k_pool.shape[0]
+    bad = case.block_table.copy()
+    bad[0, 3] = -7                   # prefix pages of sequence 0
+    bad[0, 10] = npages + 1000
+    bad[0, 700 // P] = -1            # every page sequence 0 appends to
+    bad[0, (700 + 19) // P] = npages
+    note("out-of-range page ids in sequence 0's table: csr_extend_attention(APPEND)")
+    dev = Dev(case)
+    dev.bt = torch.from_numpy(bad).cuda()
+    out, lse = dev.extend(append=True)
+    torch.cuda.synchronize()
+    n0 = int(case.seqlen_q[0])
+    assert torch.isfinite(out[:n0].float()).all() and torch.isfinite(lse[:n0]).all()
+    rows1 = np.arange(n0, case.total_q, dtype=np.int32)
+    ref, ref_lse = oracle_rows(case, rows1)
+    compare(case, out, lse, rows1, ref, ref_lse, "sequence 1 beside a bad table")
+    # expected pools: only sequence 1's chunk appended
+    cu1 = np.array([0, 0, case.total_q - n0], np.int32)
+    kp, vp = oracle.kv_append(case.k_new[n0:], case.v_new[n0:], case.k_pool, case.v_pool, case.block_table,
+                              case.bt_stride, cu1, case.cache_len, case.num_kv_heads, case.head_dim, P)
+    np.testing.assert_array_equal(from_dev(case, dev.k_pool), kp)
+    np.testing.assert_array_equal(from_dev(case, dev.v_pool), vp)
