@@ -183,12 +183,16 @@ static int owner(const int32_t* cu, int batch, int tok) {
  * pairs: [n_rows, Hq] number of (query, key) pairs evaluated.  cache_len may be
  * NULL (every L_b = 0: prefill).  rope_style != ROPE_NONE rotates each query
  * row and each chunk key (t >= L_b) at its absolute position (rope_dim dims,
- * base rope_theta); cached keys are used as stored.  Returns 0, or -1 for a
- * token outside every sequence, or -2 on allocation failure.
+ * base rope_theta); cached keys are used as stored.  kv_fp8: the pools hold
+ * e4m3 codes (dequantised by k_scale, v_scale) and chunk keys/values enter
+ * quantised as they are cached; q_scale > 0 (fp8 cache only) quantises each
+ * (rotated) query element the same way under q_scale, the fp8-product mode.
+ * Returns 0, or -1 for a token outside every sequence, or -2 on allocation
+ * failure.
  */
 int csr_oracle_attention(int dtype, int Hq, int Hkv, int d, int P, double scale, int rope_style,
                          int rope_dim, double rope_theta, int kv_fp8, float k_scale, float v_scale,
-                         int batch,
+                         float q_scale, int batch,
                          const void* q, const void* k_new, const void* v_new, const void* k_pool,
                          const void* v_pool, const int32_t* block_table, int bt_stride,
                          const int32_t* cu_seqlens_q, const int32_t* cache_len, int n_rows,
@@ -227,6 +231,8 @@ int csr_oracle_attention(int dtype, int Hq, int Hkv, int d, int P, double scale,
     for (int j = 0; j < G; ++j) {
       for (int c = 0; c < d; ++c) raw[c] = widen(q, ((int64_t)tok * Hq + g * G + j) * d + c, dtype);
       rope_row(raw, qv + j * d, d, rope_dim, rope_style, rope_theta, L + i);
+      if (kv_fp8 && q_scale > 0.f) /* fp8 products: the (rotated) query enters as e4m3 codes too */
+        for (int c = 0; c < d; ++c) qv[j * d + c] = e4m3_decode(fp8_quantize(qv[j * d + c], q_scale)) * (double)q_scale;
     }
     /* pass 1: scores */
     for (int64_t t = 0; t < nkeys; ++t) {

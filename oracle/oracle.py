@@ -37,8 +37,8 @@ def _load():
         lib = ctypes.CDLL(LIB)
         p, i, d = ctypes.c_void_p, ctypes.c_int, ctypes.c_double
         f = ctypes.c_float
-        lib.csr_oracle_attention.argtypes = [i, i, i, i, i, d, i, i, d, i, f, f, i, p, p, p, p, p, p, i, p, p, i, p,
-                                             p, p, p, i]
+        lib.csr_oracle_attention.argtypes = [i, i, i, i, i, d, i, i, d, i, f, f, f, i, p, p, p, p, p, p, i, p, p, i,
+                                             p, p, p, p, i]
         lib.csr_oracle_attention.restype = i
         lib.csr_oracle_kv_append.argtypes = [i, i, i, i, i, i, d, i, f, f, i, p, p, p, p, p, i, p, p]
         lib.csr_oracle_e4m3_encode.argtypes = [p, p, ctypes.c_int64]
@@ -118,7 +118,7 @@ def rope(x, positions, style, rotary_dims, base):
 
 def attention(dtype, q, k_new, v_new, k_pool, v_pool, block_table, bt_stride, cu_seqlens_q,
               cache_len, rows, num_q_heads, num_kv_heads, head_dim, page_size, scale=None,
-              nthreads=None, rope=None, fp8=None):
+              nthreads=None, rope=None, fp8=None, q_fp8=None):
     """Extend attention for the query tokens in ``rows`` (all heads).
 
     Paper Sec. II, eq. (causal_attention_1)-(causal_attention_3) over the
@@ -129,10 +129,14 @@ def attention(dtype, q, k_new, v_new, k_pool, v_pool, block_table, bt_stride, cu
     row and every chunk key at its absolute position (see ``rope``); cached
     keys are used as stored.  ``fp8=(k_scale, v_scale)``: the pools hold e4m3
     codes (uint8) and chunk keys/values enter quantised exactly as the append
-    stores them.  Returns ``(out [R,Hq,d] f64, lse [R,Hq] f64, pairs [R,Hq]
-    i64)``.
+    stores them.  ``q_fp8=q_scale`` (with ``fp8``): fp8 products, every
+    (rotated) query element enters as e4m3(x * fp32(1/q_scale)) * q_scale, the
+    keys' quantiser.  Returns ``(out [R,Hq,d] f64, lse [R,Hq] f64, pairs
+    [R,Hq] i64)``.
     """
     lib = _load()
+    if q_fp8 is not None and fp8 is None:
+        raise ValueError("fp8 products (q_fp8) need an fp8 cache (fp8)")
     G = num_q_heads // num_kv_heads
     if G > 64 or num_q_heads % num_kv_heads:
         raise ValueError("oracle supports Hq % Hkv == 0 and G <= 64")
@@ -147,7 +151,8 @@ def attention(dtype, q, k_new, v_new, k_pool, v_pool, block_table, bt_stride, cu
     cl = _i32(cache_len)
     rc = lib.csr_oracle_attention(
         dtype, num_q_heads, num_kv_heads, head_dim, page_size, 0.0 if scale is None else float(scale),
-        *_rope_args(rope, head_dim), *_fp8_args(fp8), int(cu.shape[0] - 1), *[_ptr(a) for a in arrs], _ptr(bt), int(bt_stride), _ptr(cu), _ptr(cl),
+        *_rope_args(rope, head_dim), *_fp8_args(fp8), 0.0 if q_fp8 is None else float(q_fp8), int(cu.shape[0] - 1),
+        *[_ptr(a) for a in arrs], _ptr(bt), int(bt_stride), _ptr(cu), _ptr(cl),
         R, _ptr(rows), _ptr(out), _ptr(lse), _ptr(pairs), int(nthreads or default_threads()))
     if rc != 0:
         raise RuntimeError(f"oracle attention failed ({rc})")

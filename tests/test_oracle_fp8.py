@@ -63,18 +63,22 @@ def torch_quant_dequant(x_bf16_bits, scale):
     return torch.from_numpy(codes).view(torch.float8_e4m3fn).to(torch.float64).numpy() * float(np.float32(scale))
 
 
+QS = 0.015625  # q_scale of the fp8-product mode in these pins
+
+
+@pytest.mark.parametrize("q_fp8", [None, QS], ids=["bf16_q", "fp8_q"])
 @pytest.mark.parametrize("kw", [
     dict(num_q_heads=8, num_kv_heads=2, head_dim=32, cache_len=[37], seqlen_q=[11], page_size=4),
     dict(num_q_heads=6, num_kv_heads=3, head_dim=16, cache_len=[5, 0, 33], seqlen_q=[3, 7, 1], page_size=2,
          interleave=True),
 ])
-def test_attention_over_an_fp8_cache_matches_sdpa(kw):
+def test_attention_over_an_fp8_cache_matches_sdpa(kw, q_fp8):
     case = dg.with_fp8_pools(dg.make_case("fp8", dtype=dg.BF16, scale=0.5, cfg_id=80, **kw), cfg_id=80)
     ks, vs = SCALES
     out, lse, _ = oracle.attention(oracle.BF16, case.q, case.k_new, case.v_new, case.k_pool, case.v_pool,
                                    case.block_table, case.bt_stride, case.cu_seqlens_q, case.cache_len,
                                    np.arange(case.total_q, dtype=np.int32), case.num_q_heads, case.num_kv_heads,
-                                   case.head_dim, case.page_size, fp8=(ks, vs))
+                                   case.head_dim, case.page_size, fp8=(ks, vs), q_fp8=q_fp8)
     G = case.num_q_heads // case.num_kv_heads
     P = case.page_size
     deq = lambda c, s: torch.from_numpy(c).view(torch.float8_e4m3fn).to(torch.float64).numpy() * float(np.float32(s))  # noqa: E731
@@ -89,7 +93,8 @@ def test_attention_over_an_fp8_cache_matches_sdpa(kw):
         vp = case.v_pool[page, t % P]
         k = np.concatenate([deq(kp, ks), torch_quant_dequant(case.k_new[lo:hi], ks)], axis=0)
         v = np.concatenate([deq(vp, vs), torch_quant_dequant(case.v_new[lo:hi], vs)], axis=0)
-        q = dg.bf16_bits_to_f32(case.q[lo:hi]).astype(np.float64)
+        q = (dg.bf16_bits_to_f32(case.q[lo:hi]).astype(np.float64) if q_fp8 is None
+             else torch_quant_dequant(case.q[lo:hi], q_fp8))
         qt = torch.from_numpy(q).permute(1, 0, 2)
         kt = torch.from_numpy(k).permute(1, 0, 2).repeat_interleave(G, dim=0)
         vt = torch.from_numpy(v).permute(1, 0, 2).repeat_interleave(G, dim=0)
@@ -146,3 +151,40 @@ def test_fp8_chunk_split_is_exact(rope):
                                              np.array([L + n1], np.int32), np.arange(n2, dtype=np.int32), *args,
                                              rope=rope, fp8=fp8)
     assert np.array_equal(second, one[n1:]) and np.array_equal(second_lse, one_lse[n1:])
+
+
+def test_fp8_products_quantise_the_rotated_query():
+    """With RoPE the query is rotated first (fp64, then fp32 as the quantiser
+    reads it) and then quantised like a key: the result equals SDPA over
+    torch-quantised rotated queries and an unrotated-cache, rotated-chunk key set."""
+    case = dg.with_fp8_pools(dg.make_case("fp8qr", dtype=dg.BF16, num_q_heads=4, num_kv_heads=2, head_dim=32,
+                                          cache_len=[19], seqlen_q=[6], page_size=4, scale=0.5, cfg_id=83),
+                             cfg_id=83)
+    ks, vs = SCALES
+    rope = (oracle.ROPE_NEOX, 0, 1e4)
+    rows = np.arange(case.total_q, dtype=np.int32)
+    args = (case.q, case.k_new, case.v_new, case.k_pool, case.v_pool, case.block_table, case.bt_stride,
+            case.cu_seqlens_q, case.cache_len, rows, case.num_q_heads, case.num_kv_heads, case.head_dim,
+            case.page_size)
+    out, lse, _ = oracle.attention(oracle.BF16, *args, rope=rope, fp8=(ks, vs), q_fp8=QS)
+    L, n, P, G = 19, 6, 4, 2
+    pos = L + np.arange(n)
+    q = oracle.rope(dg.bf16_bits_to_f32(case.q).astype(np.float64), pos, *rope)
+    qd = torch.from_numpy(torch_encode(q.astype(np.float32) * (np.float32(1) / np.float32(QS)))).view(
+        torch.float8_e4m3fn).to(torch.float64).numpy() * QS
+    t = np.arange(L)
+    page = case.block_table[0, t // P].astype(np.int64)
+    deq = lambda c, sc: torch.from_numpy(c).view(torch.float8_e4m3fn).to(torch.float64).numpy() * float(np.float32(sc))  # noqa: E731
+    kc = oracle.rope(dg.bf16_bits_to_f32(case.k_new).astype(np.float64), pos, *rope)
+    kq = deq(torch_encode(kc.astype(np.float32) * (np.float32(1) / np.float32(ks))), ks)
+    k = np.concatenate([deq(case.k_pool[page, t % P], ks), kq], axis=0)
+    v = np.concatenate([deq(case.v_pool[page, t % P], vs), torch_quant_dequant(case.v_new, vs)], axis=0)
+    qt = torch.from_numpy(qd).permute(1, 0, 2)
+    kt = torch.from_numpy(k).permute(1, 0, 2).repeat_interleave(G, dim=0)
+    vt = torch.from_numpy(v).permute(1, 0, 2).repeat_interleave(G, dim=0)
+    mask = torch.arange(L + n)[None, :] <= (L + torch.arange(n))[:, None]
+    ref = torch.nn.functional.scaled_dot_product_attention(qt, kt, vt, attn_mask=mask, scale=1 / math.sqrt(32))
+    np.testing.assert_allclose(out, ref.permute(1, 0, 2).numpy(), rtol=0, atol=1e-12)
+    # and quantising the query changes the result (the pin is not vacuous)
+    out_bf16, _, _ = oracle.attention(oracle.BF16, *args, rope=rope, fp8=(ks, vs))
+    assert np.abs(out - out_bf16).max() > 1e-4
