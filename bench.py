@@ -44,6 +44,7 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 PEAK_BF16_TFLOPS = 2500.0   # MI355X dense bf16 MFMA (published)
+PEAK_FP8_TFLOPS = 5000.0    # MI355X dense fp8 MFMA (published)
 PEAK_F32_TFLOPS = 157.3     # MI355X fp32 matrix (published)
 PEAK_HBM_GBS = 8000.0       # MI355X HBM3E (published)
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic_extend_attn.json")
@@ -316,6 +317,8 @@ def main():
     ap.add_argument("--kv", choices=("same", "fp8"), default="same",
                     help="fp8: the cache holds OCP e4m3 codes (k_scale 0.0625, v_scale 0.0390625); the chunk is "
                          "quantised inside the step")
+    ap.add_argument("--qk", choices=("bf16", "fp8"), default="bf16",
+                    help="fp8 (with --kv fp8): fp8 score products, q quantised under q_scale 1/64")
     ap.add_argument("--asr-period-ms", type=float, default=2.0, help="asr: task arrival period")
     ap.add_argument("--asr-secondary-cus-per-xcd", type=int, default=8, help="asr: secondary partition size")
     ap.add_argument("--asr-tau", type=int, default=110000, help="asr: eviction threshold tau_mem (tokens)")
@@ -351,9 +354,13 @@ def main():
     t0 = time.perf_counter()
     case = dg.config(args.workload)
     fp8 = args.kv == "fp8"
+    qk8 = args.qk == "fp8"
+    if qk8 and not fp8:
+        print("--qk fp8 needs --kv fp8", file=sys.stderr)
+        sys.exit(2)
     if fp8:
         case = dg.with_fp8_pools(case, cfg_id=603)   # random e4m3 codes for the cached prefix
-    wl_name = args.workload + ("_fp8" if fp8 else "")
+    wl_name = args.workload + ("_fp8" if fp8 else "") + ("qk" if qk8 else "")
     log(f"workload {args.workload}: L={case.cache_len.tolist()} n={case.seqlen_q.tolist()} "
         f"Hq={case.num_q_heads} Hkv={case.num_kv_heads} d={case.head_dim} P={case.page_size} "
         f"({time.perf_counter() - t0:.1f}s to generate)")
@@ -380,9 +387,11 @@ def main():
                          torch.bfloat16 if bf16 else torch.float32, rope_style=rope_style, rope_dim=args.rope_dim,
                          rope_theta=args.rope_theta if rope_style else 0.0,
                          kv_dtype=csr.CSR_KV_FP8_E4M3 if fp8 else csr.CSR_KV_SAME,
-                         k_scale=0.0625 if fp8 else 0.0, v_scale=0.0390625 if fp8 else 0.0)
-    if fp8:  # the unrotated comparison keeps the fp8 cache
+                         k_scale=0.0625 if fp8 else 0.0, v_scale=0.0390625 if fp8 else 0.0,
+                         q_scale=0.015625 if qk8 else 0.0)
+    if fp8:  # the unrotated comparison keeps the fp8 cache (and the fp8 scores)
         plain_desc.kv_dtype, plain_desc.k_scale, plain_desc.v_scale = csr.CSR_KV_FP8_E4M3, 0.0625, 0.0390625
+        plain_desc.q_scale = 0.015625 if qk8 else 0.0
     out = torch.empty_like(q)
     lse = torch.empty((case.total_q, case.num_q_heads), dtype=torch.float32, device="cuda")
     if prefill_mode:
@@ -435,6 +444,8 @@ def main():
     flops = case.flops()
     value = flops / (ms_per_step * 1e-3) / 1e12
     peak = PEAK_BF16_TFLOPS if bf16 else PEAK_F32_TFLOPS
+    if qk8:  # equal FLOPs in QK^T (fp8 peak) and PV (bf16 peak): the time-weighted peak of the pair
+        peak = 1.0 / (0.5 / PEAK_FP8_TFLOPS + 0.5 / PEAK_BF16_TFLOPS)
     achieved = flops / (attn_avg * 1e-3) / 1e12
     log(f"{args.steps} steps: {ms_per_step:.4f} ms/step ({value:.1f} TFLOP/s); attention kernel avg "
         f"{attn_avg:.4f} ms (min {min(attn_ms):.4f}) = {achieved:.1f} TFLOP/s = {100 * achieved / peak:.1f}% of peak")
@@ -451,7 +462,7 @@ def main():
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
-        "dtype": "bf16" if bf16 else "f32",
+        "dtype": ("fp8 QK^T + bf16 PV" if qk8 else "bf16") if bf16 else "f32",
         "data": "synthetic",
         "config": {
             "workload": (f"{'re-prefill' if prefill_mode else 'extend'} one layer: L={case.max_cache_len} cached "
@@ -460,6 +471,7 @@ def main():
                          f"{'kv append + ' if not prefill_mode else 'cache write + '}attention (+ split-K merge)"),
             "name": wl_name,
             "kv_cache": "fp8 e4m3, per-tensor scales (k 0.0625, v 0.0390625)" if fp8 else "input type",
+            "scores": "fp8 products (q e4m3 under q_scale 0.015625)" if qk8 else "bf16 products",
             "global_batch": case.batch,
             "seq_len": int(case.max_cache_len + case.max_seqlen_q),
             "chunk_tokens": case.total_q,
@@ -474,7 +486,8 @@ def main():
             "unit": "TFLOP/s",
             "frac": round(achieved / peak, 4),
             "traffic": traffic,
-            "kernel": ("attn_bf16_kernel<fp8 K/V>" if fp8 else "attn_bf16_kernel") if bf16 else "attn_f32_kernel",
+            "kernel": (("attn_bf16_kernel<fp8 K/V, fp8 scores>" if qk8 else "attn_bf16_kernel<fp8 K/V>") if fp8
+                       else "attn_bf16_kernel") if bf16 else "attn_f32_kernel",
             "kernel_ms": round(attn_avg, 5),
             "hbm_gbs_algorithmic": round(abytes / (attn_avg * 1e-3) / 1e9, 1),
         },

@@ -41,6 +41,12 @@
  * whether it comes from the chunk or, on a later call, from the cache.  The
  * attention converts codes to bf16 exactly and computes as for bf16 (fp32
  * accumulation); q and the output stay bf16.  Needs dtype CSR_BF16, d = 128.
+ * FP8 score products (q_scale > 0): each (rotated) query element is
+ * quantised by the same rule under q_scale, e4m3_nearest_even(clamp(
+ * x * fp32(1 / q_scale), -448, 448)), and the scores are q_scale * k_scale *
+ * sum of code products, evaluated on the fp8 matrix cores with fp32
+ * accumulation; the probabilities and values stay bf16.  The caller picks
+ * q_scale so that |q| / q_scale stays within 448.
  *
  * Memory layout (all row-major, element type per csr_attn_desc.dtype):
  *   q                 [T_q][Hq][d]        T_q = cu_seqlens_q[batch]
@@ -129,6 +135,8 @@ typedef struct {
   int32_t kv_dtype;      /* csr_kv_dtype; 0 = the cache holds the input type */
   float k_scale;         /* fp8 cache: key dequantisation scale, finite and > 0 */
   float v_scale;         /* fp8 cache: value dequantisation scale, finite and > 0 */
+  float q_scale;         /* fp8 cache only: > 0 selects fp8 score products (q quantised under
+                            this scale like the keys); 0 = bf16 q */
 } csr_attn_desc;
 
 /*

@@ -31,7 +31,8 @@ class AttnDesc(ctypes.Structure):
     _fields_ = [("num_q_heads", ctypes.c_int32), ("num_kv_heads", ctypes.c_int32), ("head_dim", ctypes.c_int32),
                 ("page_size", ctypes.c_int32), ("softmax_scale", ctypes.c_float), ("dtype", ctypes.c_int32),
                 ("rope_style", ctypes.c_int32), ("rope_dim", ctypes.c_int32), ("rope_theta", ctypes.c_float),
-                ("kv_dtype", ctypes.c_int32), ("k_scale", ctypes.c_float), ("v_scale", ctypes.c_float)]
+                ("kv_dtype", ctypes.c_int32), ("k_scale", ctypes.c_float), ("v_scale", ctypes.c_float),
+                ("q_scale", ctypes.c_float)]
 
 
 class CsrError(RuntimeError):
@@ -92,14 +93,16 @@ def set_attention_events(begin_event, end_event) -> None:
 def make_desc(num_q_heads: int, num_kv_heads: int, head_dim: int, page_size: int = 16, dtype=torch.bfloat16,
               softmax_scale: float = 0.0, rope_style: int = CSR_ROPE_NONE, rope_dim: int = 0,
               rope_theta: float = 0.0, kv_dtype: int = CSR_KV_SAME, k_scale: float = 0.0,
-              v_scale: float = 0.0) -> AttnDesc:
+              v_scale: float = 0.0, q_scale: float = 0.0) -> AttnDesc:
     """csr_attn_desc.  ``rope_style`` != CSR_ROPE_NONE makes the library rotate q
     and k_new at their absolute positions (``rope_dim`` dims, 0 = all; base
     ``rope_theta``); ``kv_dtype`` = CSR_KV_FP8_E4M3 keeps the cache as e4m3
-    codes (uint8 pools) with dequantisation scales ``k_scale``, ``v_scale``."""
+    codes (uint8 pools) with dequantisation scales ``k_scale``, ``v_scale``;
+    with it, ``q_scale`` > 0 selects fp8 score products (q quantised too)."""
     dt = {torch.bfloat16: CSR_BF16, torch.float32: CSR_F32}.get(dtype, dtype)
     return AttnDesc(num_q_heads, num_kv_heads, head_dim, page_size, softmax_scale, int(dt), int(rope_style),
-                    int(rope_dim), float(rope_theta), int(kv_dtype), float(k_scale), float(v_scale))
+                    int(rope_dim), float(rope_theta), int(kv_dtype), float(k_scale), float(v_scale),
+                    float(q_scale))
 
 
 def _ptr(t: Optional[torch.Tensor]):

@@ -70,11 +70,20 @@ csr_status check_desc(const csr_attn_desc* d) {
     if (!(d->k_scale > 0.f) || isinf(d->k_scale) || !(d->v_scale > 0.f) || isinf(d->v_scale))
       return fail(CSR_E_INVAL, "k_scale and v_scale must be finite and > 0");
   }
+  if (d->q_scale != 0.f) {
+    if (d->kv_dtype != CSR_KV_FP8_E4M3)
+      return fail(CSR_E_UNSUPPORTED, "fp8 score products (q_scale) need an fp8 cache");
+    if (!(d->q_scale > 0.f) || isinf(d->q_scale)) return fail(CSR_E_INVAL, "q_scale must be 0, or finite and > 0");
+  }
   return CSR_OK;
 }
 
 bool has_rope(const csr_attn_desc* d) { return d->rope_style != CSR_ROPE_NONE; }
 bool kv_fp8(const csr_attn_desc* d) { return d->kv_dtype == CSR_KV_FP8_E4M3; }
+// fp8 score products: q quantised like the keys, Q K^T on the fp8 matrix cores.
+bool qk_fp8(const csr_attn_desc* d) { return kv_fp8(d) && d->q_scale > 0.f; }
+// The attention reads q from the workspace: rotated (RoPE) and/or quantised (fp8 products).
+bool prep_q(const csr_attn_desc* d) { return has_rope(d) || qk_fp8(d); }
 // RoPE or an fp8 cache: one launch prepares q/k/v (and appends) before the attention.
 bool needs_prep(const csr_attn_desc* d) { return has_rope(d) || kv_fp8(d); }
 
@@ -82,8 +91,9 @@ size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 
 int elem_bytes(const csr_attn_desc* d) { return d->dtype == CSR_BF16 ? 2 : 4; }
 
-// Workspace head written by the prep launch, each part 256-aligned: rotated q
-// (RoPE only), prepared k (rotated and/or quantised), quantised v (fp8 only).
+// Workspace head written by the prep launch, each part 256-aligned: prepared q
+// (rotated with RoPE, e4m3 codes with fp8 products), prepared k (rotated
+// and/or quantised), quantised v (fp8 only).
 struct PrepLayout {
   size_t q_off, k_off, v_off, bytes;
 };
@@ -91,7 +101,7 @@ PrepLayout prep_layout(const csr_attn_desc* d, int total) {
   PrepLayout l{0, 0, 0, 0};
   if (!needs_prep(d)) return l;
   const size_t rows = (size_t)total * d->head_dim;
-  const size_t qb = has_rope(d) ? align256(rows * d->num_q_heads * elem_bytes(d)) : 0;
+  const size_t qb = prep_q(d) ? align256(rows * d->num_q_heads * (qk_fp8(d) ? 1 : elem_bytes(d))) : 0;
   const size_t kb = align256(rows * d->num_kv_heads * (kv_fp8(d) ? 1 : elem_bytes(d)));
   const size_t vb = kv_fp8(d) ? align256(rows * d->num_kv_heads) : 0;
   l.q_off = 0;
@@ -107,10 +117,12 @@ csr::RopeArgs rope_args(const csr_attn_desc* d, int batch, const void* q, const 
                         void* k_out, void* v_out, void* k_pool, void* v_pool, int num_pages, const int32_t* bt,
                         int bt_stride, const int32_t* cu, const int32_t* cache_len, int total) {
   csr::RopeArgs a;
-  a.q = has_rope(d) ? q : nullptr;
+  a.q = prep_q(d) ? q : nullptr;
   a.k = k;
   a.v = v;
-  a.q_out = has_rope(d) ? q_out : nullptr;
+  a.q_out = prep_q(d) ? q_out : nullptr;
+  a.q8 = qk_fp8(d) ? 1 : 0;
+  a.inv_q = qk_fp8(d) ? 1.f / d->q_scale : 1.f;
   a.k_out = k_out;
   a.v_out = kv_fp8(d) ? v_out : nullptr;
   a.kv8 = kv_fp8(d) ? 1 : 0;
@@ -322,8 +334,9 @@ csr_status run_attention(const csr_attn_desc* d, int batch, const void* q, const
   a.log2P = ilog2(d->page_size);
   // an fp8 cache holds K / k_scale and V / v_scale: the scales come back in the
   // score scale and in the output
-  a.scale_log2 = scale * 1.4426950408889634f * (kv_fp8(d) ? d->k_scale : 1.f);
+  a.scale_log2 = scale * 1.4426950408889634f * (kv_fp8(d) ? d->k_scale : 1.f) * (qk_fp8(d) ? d->q_scale : 1.f);
   a.v_scale = kv_fp8(d) ? d->v_scale : 1.f;
+  a.qk8 = qk_fp8(d) ? 1 : 0;
   a.kv_fp8 = kv_fp8(d) ? 1 : 0;
   a.four_waves = p.four_waves;
   a.dma_upper = p.dma_upper;
@@ -477,13 +490,13 @@ csr_status csr_extend_attention(const csr_attn_desc* desc, int32_t batch, const 
     // v_new into the workspace (and appends); the attention then reads the
     // prepared copies.
     char* ws = static_cast<char*>(workspace);
-    const bool rope = has_rope(desc), fp8 = kv_fp8(desc);
+    const bool pq = prep_q(desc), fp8 = kv_fp8(desc);
     const csr::RopeArgs r = rope_args(desc, batch, q, k_new, v_new, ws + pl.q_off, ws + pl.k_off, ws + pl.v_off,
                                       append ? k_pool : nullptr, append ? v_pool : nullptr, num_pages, block_table,
                                       bt_stride, cu_seqlens_q, cache_seqlens, total_q);
     st = launched(csr::launch_rope_append(r, desc->dtype == CSR_BF16, s), "prep");
     if (st != CSR_OK) return st;
-    return run_attention(desc, batch, rope ? ws + pl.q_off : q, ws + pl.k_off, fp8 ? ws + pl.v_off : v_new, k_pool,
+    return run_attention(desc, batch, pq ? ws + pl.q_off : q, ws + pl.k_off, fp8 ? ws + pl.v_off : v_new, k_pool,
                          v_pool, num_pages, block_table, bt_stride, cu_seqlens_q,
                          max_cache_len > 0 ? cache_seqlens : nullptr, total_q, max_seqlen_q, max_cache_len, out, lse,
                          p.ws_bytes ? ws + pl.bytes : nullptr, workspace_bytes - pl.bytes, s);
@@ -521,13 +534,13 @@ csr_status csr_prefill(const csr_attn_desc* desc, int32_t batch, const void* q, 
   hipStream_t s = static_cast<hipStream_t>(stream);
   if (pl.bytes > 0) {
     char* ws = static_cast<char*>(workspace);
-    const bool rope = has_rope(desc), fp8 = kv_fp8(desc);
+    const bool pq = prep_q(desc), fp8 = kv_fp8(desc);
     const csr::RopeArgs r = rope_args(desc, batch, q, k, v, ws + pl.q_off, ws + pl.k_off, ws + pl.v_off,
                                       write_cache ? k_pool : nullptr, write_cache ? v_pool : nullptr, num_pages,
                                       block_table, bt_stride, cu_seqlens, nullptr, total);
     st = launched(csr::launch_rope_append(r, desc->dtype == CSR_BF16, s), "prep");
     if (st != CSR_OK) return st;
-    return run_attention(desc, batch, rope ? ws + pl.q_off : q, ws + pl.k_off, fp8 ? ws + pl.v_off : v, nullptr,
+    return run_attention(desc, batch, pq ? ws + pl.q_off : q, ws + pl.k_off, fp8 ? ws + pl.v_off : v, nullptr,
                          nullptr, 0, nullptr, 1, cu_seqlens, nullptr, total, max_seqlen, 0, out, lse,
                          p.ws_bytes ? ws + pl.bytes : nullptr, workspace_bytes - pl.bytes, s);
   }

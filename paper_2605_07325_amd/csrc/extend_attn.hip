@@ -56,6 +56,7 @@ typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
 typedef short s16x4 __attribute__((ext_vector_type(4)));
 typedef __attribute__((address_space(3))) s16x4 lds_s16x4;
 typedef int32_t i32x2 __attribute__((ext_vector_type(2)));
+typedef int32_t i32x8 __attribute__((ext_vector_type(8)));
 typedef __attribute__((address_space(3))) i32x2 lds_i32x2;
 
 
@@ -257,11 +258,18 @@ struct TileLoader {
 // half of the waves): the upper half, which has no rows, issues all of the
 // K/V DMA and the computing waves none, so the DMA issue stalls stay off the
 // computing waves' per-tile dependency chain.
-template <int D, bool SCALAR_PAGES, bool KV8 = false, int NW = 8, bool DMA_UPPER = false>
+//
+// QK8 (fp8 score products, with KV8): q arrives as e4m3 codes and the scores
+// of a 32-key block are two v_mfma_f32_32x32x64_f8f6f4 (d 0..63, 64..127).
+// In that instruction lane r + 32h of either operand holds 32 bytes, and A
+// and B pair the same byte slots (probed), so both take d = 64i + 32h + b:
+// two 16-byte chunks of the key row in LDS, two of the query row.
+template <int D, bool SCALAR_PAGES, bool KV8 = false, int NW = 8, bool DMA_UPPER = false, bool QK8 = false>
 __global__ void __launch_bounds__(NW * 64, 8 / NW) attn_bf16_kernel(const AttnArgs a) {
   static_assert(!KV8 || D == 128, "fp8 K/V rows are laid out for d = 128");
   static_assert(NW == 8 || (NW == 4 && KV8), "4-wave workgroups only with the 64 KB fp8 rings");
-  typedef typename KFragT<KV8>::type KF;  // one K fragment as read from LDS
+  static_assert(!QK8 || KV8, "fp8 score products need the fp8 cache");
+  typedef typename KFragT<KV8 && !QK8>::type KF;  // one K fragment as read from LDS
   constexpr int BM = NW * 32;
   constexpr int ROWB = D * (KV8 ? 1 : 2);  // bytes per key row (bf16 or e4m3 codes)
   constexpr int NCH = ROWB / 16;
@@ -304,8 +312,10 @@ __global__ void __launch_bounds__(NW * 64, 8 / NW) attn_bf16_kernel(const AttnAr
   const int kv_stride = a.Hkv * ROWB;  // bytes between consecutive tokens of one kv head
   const int last_key = u.kv_end - 1;
 
-  // Q^T fragment: lane holds packed row (l32), d = ds*16 + 8h .. +7.
-  u32x4 qf[DS];
+  // Q^T fragment: lane holds packed row (l32), d = ds*16 + 8h .. +7 (bf16);
+  // QK8: e4m3 codes of d = 64i + 32h + 16j .. +15 in qf[2i + j].
+  constexpr int NQF = QK8 ? 4 : DS;
+  u32x4 qf[NQF];
   const int m_row = u.m0 + wave * 32 + l32;
   const bool valid = m_row < u.rows_total;
   // A wave whose 32 rows are all padding (short chunks: n*G < BM) skips the
@@ -316,11 +326,18 @@ __global__ void __launch_bounds__(NW * 64, 8 / NW) attn_bf16_kernel(const AttnAr
   const int lim = u.L + tok;  // last key this lane's row sees
   {
     const int j = m_row - tok * G;
-    const char* qrow =
-        static_cast<const char*>(a.q) + (((int64_t)(u.cuq + tok) * a.Hq + u.g * G + j) * D + h * 8) * 2;
+    if constexpr (QK8) {
+      const char* qrow = static_cast<const char*>(a.q) + ((int64_t)(u.cuq + tok) * a.Hq + u.g * G + j) * D + h * 32;
 #pragma unroll
-    for (int ds = 0; ds < DS; ++ds)
-      qf[ds] = valid ? *reinterpret_cast<const u32x4*>(qrow + ds * 32) : u32x4{0, 0, 0, 0};
+      for (int x = 0; x < 4; ++x)
+        qf[x] = valid ? *reinterpret_cast<const u32x4*>(qrow + 64 * (x >> 1) + 16 * (x & 1)) : u32x4{0, 0, 0, 0};
+    } else {
+      const char* qrow =
+          static_cast<const char*>(a.q) + (((int64_t)(u.cuq + tok) * a.Hq + u.g * G + j) * D + h * 8) * 2;
+#pragma unroll
+      for (int ds = 0; ds < DS; ++ds)
+        qf[ds] = valid ? *reinterpret_cast<const u32x4*>(qrow + ds * 32) : u32x4{0, 0, 0, 0};
+    }
   }
 
   // ---- DMA: lane's key row within the tile for block j, and its byte offset inside a token row.
@@ -407,11 +424,17 @@ __global__ void __launch_bounds__(NW * 64, 8 / NW) attn_bf16_kernel(const AttnAr
   const uint32_t vring_addr = (uint32_t)(size_t)((__attribute__((address_space(3))) char*)vring);
 
   // Per-lane LDS read offsets (stage and 32-key block offsets are added as immediates).
-  int koff[DS];
+  // QK8: koff[2i + j] = 16-byte chunk 4i + 2h + j of the key row (d = 64i + 32h + 16j ..).
+  int koff[QK8 ? 4 : DS];
+  if constexpr (QK8) {
 #pragma unroll
-  for (int ds = 0; ds < DS; ++ds)
-    koff[ds] = KV8 ? l32 * ROWB + (slot<NCH, true>(l32, ds) << 4) + 8 * h  // 8 codes: d = 16 ds + 8h ..
-                   : l32 * ROWB + (slot<NCH>(l32, ds * 2 + h) << 4);
+    for (int x = 0; x < 4; ++x) koff[x] = l32 * ROWB + (slot<NCH, true>(l32, 4 * (x >> 1) + 2 * h + (x & 1)) << 4);
+  } else {
+#pragma unroll
+    for (int ds = 0; ds < DS; ++ds)
+      koff[ds] = KV8 ? l32 * ROWB + (slot<NCH, true>(l32, ds) << 4) + 8 * h  // 8 codes: d = 16 ds + 8h ..
+                     : l32 * ROWB + (slot<NCH>(l32, ds * 2 + h) << 4);
+  }
   const int grp = lane >> 4, rr = (lane & 15) >> 2, qq = lane & 3, hh = grp >> 1;
   int voff_a[DB], voff_b[DB];
   {
@@ -447,23 +470,55 @@ __global__ void __launch_bounds__(NW * 64, 8 / NW) attn_bf16_kernel(const AttnAr
 
   // Scores of 32-key block kb of a K tile: S^T[key][row] (contraction steps [d0, d1)).
   // K fragments of k-steps [d0, d0 + DS/2) of block kb, and the score MFMAs over them.
+  // QK8: one fp8 product over d = 64i .. 64i + 63 from the two key chunks k0, k1.
+  auto mfma8 = [&](const u32x4& k0, const u32x4& k1, int i, f32x16& s) {
+    if constexpr (QK8) {
+      const i32x8 kv = {(int)k0[0], (int)k0[1], (int)k0[2], (int)k0[3],
+                        (int)k1[0], (int)k1[1], (int)k1[2], (int)k1[3]};
+      const u32x4 q0 = qf[2 * i], q1 = qf[2 * i + 1];
+      const i32x8 qv = {(int)q0[0], (int)q0[1], (int)q0[2], (int)q0[3],
+                        (int)q1[0], (int)q1[1], (int)q1[2], (int)q1[3]};
+      // operand formats 0, 0: e4m3 x e4m3; no block scales
+      s = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(kv, qv, s, 0, 0, 0, 0, 0, 0);
+    }
+  };
+  // K fragments of k-steps [d0, d0 + DS/2) of block kb (QK8: the two chunks of
+  // product d0 == 0 ? 0 : 1), and the score MFMAs over them.
   auto load_k = [&](const char* kl, int kb, int d0, KF* kf) {
+    if constexpr (QK8) {
+      const int i = d0 ? 1 : 0;
+      kf[0] = *reinterpret_cast<const KF*>(kl + kb * 32 * ROWB + koff[2 * i]);
+      kf[1] = *reinterpret_cast<const KF*>(kl + kb * 32 * ROWB + koff[2 * i + 1]);
+    } else {
 #pragma unroll
-    for (int i = 0; i < DS / 2; ++i) kf[i] = *reinterpret_cast<const KF*>(kl + kb * 32 * ROWB + koff[d0 + i]);
+      for (int i = 0; i < DS / 2; ++i) kf[i] = *reinterpret_cast<const KF*>(kl + kb * 32 * ROWB + koff[d0 + i]);
+    }
   };
   auto mfma_k = [&](const KF* kf, int d0, f32x16& s) {
+    if constexpr (QK8) {
+      mfma8(kf[0], kf[1], d0 ? 1 : 0, s);
+    } else {
 #pragma unroll
-    for (int i = 0; i < DS / 2; ++i)
-      s = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, kfrag(kf[i])),
-                                                  __builtin_bit_cast(bf16x8, qf[d0 + i]), s, 0, 0, 0);
+      for (int i = 0; i < DS / 2; ++i)
+        s = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, kfrag(kf[i])),
+                                                    __builtin_bit_cast(bf16x8, qf[d0 + i]), s, 0, 0, 0);
+    }
   };
   auto qk = [&](const char* kl, int kb, f32x16& s) {
     s = f32x16{};
+    if constexpr (QK8) {
+      KF kf[4];
 #pragma unroll
-    for (int ds = 0; ds < DS; ++ds) {
-      const KF kf = *reinterpret_cast<const KF*>(kl + kb * 32 * ROWB + koff[ds]);
-      s = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, kfrag(kf)),
-                                                  __builtin_bit_cast(bf16x8, qf[ds]), s, 0, 0, 0);
+      for (int x = 0; x < 4; ++x) kf[x] = *reinterpret_cast<const KF*>(kl + kb * 32 * ROWB + koff[x]);
+      mfma8(kf[0], kf[1], 0, s);
+      mfma8(kf[2], kf[3], 1, s);
+    } else {
+#pragma unroll
+      for (int ds = 0; ds < DS; ++ds) {
+        const KF kf = *reinterpret_cast<const KF*>(kl + kb * 32 * ROWB + koff[ds]);
+        s = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, kfrag(kf)),
+                                                    __builtin_bit_cast(bf16x8, qf[ds]), s, 0, 0, 0);
+      }
     }
   };
   // O^T += V^T P^T for 32-key block kb.  Contraction slot 8h+s of half hf is
@@ -946,12 +1001,14 @@ int attn_block_m(int dtype_bf16, int d, int four_waves) {
 namespace {
 
 // One bf16-Q kernel variant, with the DMA issued by every wave or by the upper half only.
-template <int D, bool SCALAR_PAGES, bool KV8, int NW>
+template <int D, bool SCALAR_PAGES, bool KV8, int NW, bool QK8 = false>
 void launch_bf16(const AttnArgs& a, unsigned grid, hipStream_t stream) {
   if (a.dma_upper)
-    hipLaunchKernelGGL((attn_bf16_kernel<D, SCALAR_PAGES, KV8, NW, true>), dim3(grid), dim3(NW * 64), 0, stream, a);
+    hipLaunchKernelGGL((attn_bf16_kernel<D, SCALAR_PAGES, KV8, NW, true, QK8>), dim3(grid), dim3(NW * 64), 0, stream,
+                       a);
   else
-    hipLaunchKernelGGL((attn_bf16_kernel<D, SCALAR_PAGES, KV8, NW, false>), dim3(grid), dim3(NW * 64), 0, stream, a);
+    hipLaunchKernelGGL((attn_bf16_kernel<D, SCALAR_PAGES, KV8, NW, false, QK8>), dim3(grid), dim3(NW * 64), 0, stream,
+                       a);
 }
 
 }  // namespace
@@ -963,12 +1020,24 @@ hipError_t launch_attention(const AttnArgs& a, int dtype_bf16, hipStream_t strea
   else if (a.xcd_remap) grid = (grid + 7u) & ~7u;
   if (dtype_bf16 && a.kv_fp8 && a.four_waves) {
     // fp8 rows, 4 waves: still 8 keys per 1 KB DMA block
-    if (a.P >= 8) launch_bf16<128, true, true, 4>(a, grid, stream);
-    else launch_bf16<128, false, true, 4>(a, grid, stream);
+    if (a.qk8) {
+      if (a.P >= 8) launch_bf16<128, true, true, 4, true>(a, grid, stream);
+      else launch_bf16<128, false, true, 4, true>(a, grid, stream);
+    } else {
+      if (a.P >= 8) launch_bf16<128, true, true, 4>(a, grid, stream);
+      else launch_bf16<128, false, true, 4>(a, grid, stream);
+    }
   } else if (dtype_bf16 && a.kv_fp8) {
     // fp8 rows: 8 keys per DMA block (more than 128 packed rows: every wave computes)
-    if (a.P >= 8) hipLaunchKernelGGL((attn_bf16_kernel<128, true, true>), dim3(grid), dim3(512), 0, stream, a);
-    else hipLaunchKernelGGL((attn_bf16_kernel<128, false, true>), dim3(grid), dim3(512), 0, stream, a);
+    if (a.qk8) {
+      if (a.P >= 8)
+        hipLaunchKernelGGL((attn_bf16_kernel<128, true, true, 8, false, true>), dim3(grid), dim3(512), 0, stream, a);
+      else
+        hipLaunchKernelGGL((attn_bf16_kernel<128, false, true, 8, false, true>), dim3(grid), dim3(512), 0, stream, a);
+    } else {
+      if (a.P >= 8) hipLaunchKernelGGL((attn_bf16_kernel<128, true, true>), dim3(grid), dim3(512), 0, stream, a);
+      else hipLaunchKernelGGL((attn_bf16_kernel<128, false, true>), dim3(grid), dim3(512), 0, stream, a);
+    }
   } else if (dtype_bf16) {
     // Scalar page-id loads need every DMA block (4 keys at d=128, 8 at d=64) inside one page.
     const bool scalar_pages = a.P >= (a.d == 128 ? 4 : 8);

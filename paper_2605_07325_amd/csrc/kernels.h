@@ -28,6 +28,7 @@ struct AttnArgs {
   float v_scale;             // output multiplier: 1, or v_scale for an fp8 cache
   int32_t kv_fp8;            // K/V (pool and chunk) are OCP e4m3 codes (bf16 q, d = 128)
   int32_t four_waves;        // fp8 only: 4-wave workgroups of 128 rows, two per CU
+  int32_t qk8;               // fp8 only: q holds e4m3 codes, Q K^T on the fp8 MFMA
   int32_t dma_upper;         // bf16 Q: all rows in the lower half of the waves; the upper half loads K/V
   int32_t batch, total_q;
   int32_t mtiles;            // packed-row tiles per (sequence, kv head)
@@ -98,7 +99,8 @@ struct RopeArgs {
   int32_t rdim;              // rotated dims, multiple of 16, <= d (0: no rotation)
   int32_t style;             // 0 none, 1 neox (i, i + r/2), 2 interleaved (2i, 2i + 1)
   int32_t kv8;               // keys/values (outputs and cache) are e4m3 codes; bf16 inputs
-  float inv_k, inv_v;        // fp32(1 / k_scale), fp32(1 / v_scale)
+  int32_t q8;                // kv8 only: q rows are quantised too (q_out holds e4m3 codes)
+  float inv_k, inv_v, inv_q;  // fp32(1 / k_scale), fp32(1 / v_scale), fp32(1 / q_scale)
   double half_turns[64];     // theta_i / pi for i < rdim / 2
 };
 hipError_t launch_rope_append(const RopeArgs& a, int dtype_bf16, hipStream_t stream);

@@ -5,7 +5,9 @@
 // With an fp8 cache each key (after its rotation) and value is stored as
 // e4m3(clamp(x * inv_scale, +-448)), nearest even, inv_scale = fp32(1/scale);
 // the quantised chunk rows also go to the workspace, so the attention reads a
-// chunk key exactly as later calls will read it from the cache.
+// chunk key exactly as later calls will read it from the cache.  In the
+// fp8-product mode the (rotated) query rows are quantised the same way into
+// the workspace (without RoPE they are only quantised: no pair is rotated).
 //
 // Chunk row i of sequence b sits at position pos = L_b + i, fixed for as long
 // as the row stays cached (prefix stability, Theorem 1), so its query and key
@@ -148,9 +150,11 @@ __device__ __forceinline__ void rotate_piece(const RopeArgs& a, const f32x2* cs,
   void* out = is_q ? a.q_out : a.k_out;
   void* pool = is_q ? nullptr : (slot >= 0 ? a.k_pool : nullptr);
   const int64_t prow = is_q ? 0 : (slot * a.Hkv + h) * d;
-  const bool quant = KV8 && !is_q;  // keys of an fp8 cache are stored as codes
+  // Keys of an fp8 cache are stored as codes; so are queries in the fp8-product mode.
+  const bool quant = KV8 && (!is_q || a.q8);
+  const float inv = is_q ? a.inv_q : a.inv_k;
   auto put = [&](void* base, int64_t e, const float (&y)[8]) {
-    if (quant) store8q(base, e, y, a.inv_k);
+    if (quant) store8q(base, e, y, inv);
     else store8<BF16>(base, e, y);
   };
   if (piece >= n_rot) {  // dims >= r: unchanged (quantised for an fp8 cache)

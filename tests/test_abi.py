@@ -182,6 +182,9 @@ def test_rope_workspace_holds_rotated_q_and_k():
     (dict(kv_dtype=csr.CSR_KV_FP8_E4M3, k_scale=1.0, v_scale=float("nan")), csr.CSR_E_INVAL),
     (dict(kv_dtype=csr.CSR_KV_FP8_E4M3, k_scale=1.0, v_scale=1.0, head_dim=64), csr.CSR_E_UNSUPPORTED),
     (dict(kv_dtype=csr.CSR_KV_FP8_E4M3, k_scale=1.0, v_scale=1.0, dtype=torch.float32), csr.CSR_E_UNSUPPORTED),
+    (dict(q_scale=0.5), csr.CSR_E_UNSUPPORTED),                                            # fp8 products, bf16 cache
+    (dict(kv_dtype=csr.CSR_KV_FP8_E4M3, k_scale=1.0, v_scale=1.0, q_scale=-1.0), csr.CSR_E_INVAL),
+    (dict(kv_dtype=csr.CSR_KV_FP8_E4M3, k_scale=1.0, v_scale=1.0, q_scale=float("inf")), csr.CSR_E_INVAL),
 ])
 def test_fp8_cache_descriptor_validation(over, code):
     assert call_extend(good_desc(**over)) == code
@@ -205,3 +208,9 @@ def test_fp8_cache_workspace_holds_quantised_chunk():
         assert csr.extend_workspace_size(fp8, 1, T, T, L) - base == extra + 2 * align(T * 4 * 128)
         assert (csr.extend_workspace_size(both, 1, T, T, L) - base
                 == extra + align(T * 64 * 128 * 2) + 2 * align(T * 4 * 128))
+        # fp8 score products: the query as e4m3 codes (one byte), with or without RoPE
+        for over in (dict(), dict(rope_style=csr.CSR_ROPE_NEOX, rope_theta=1e6)):
+            q8 = good_desc(num_q_heads=64, num_kv_heads=4, kv_dtype=csr.CSR_KV_FP8_E4M3, k_scale=0.05, v_scale=0.05,
+                           q_scale=0.015625, **over)
+            assert (csr.extend_workspace_size(q8, 1, T, T, L) - base
+                    == extra + align(T * 64 * 128) + 2 * align(T * 4 * 128))

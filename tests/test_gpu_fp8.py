@@ -1,4 +1,4 @@
-"""GPU parity for the FP8 (OCP e4m3) KV cache.
+"""GPU parity for the FP8 (OCP e4m3) KV cache and the fp8 score products.
 
 The cache holds e4m3 codes with per-tensor scales; the chunk's bf16 keys and
 values are quantised by the fused prep launch (and appended); the attention
@@ -6,7 +6,10 @@ converts codes to bf16 exactly and computes as the bf16 path does.  The
 oracle evaluates the same definition in fp64 (codes decoded exactly, chunk
 quantised by its own encoder), so outputs meet the bf16 gates and appended
 codes are compared bit for bit (with RoPE the rotation is fp32 on the GPU and
-fp64 in the oracle, so a code may rarely sit one step away).
+fp64 in the oracle, so a code may rarely sit one step away).  In the fp8-
+product mode (q_scale) the query is quantised by the same rule, on the GPU by
+the prep launch and in the oracle by its own encoder, and the scores run on
+the fp8 matrix cores; the outputs meet the same gates.
 """
 import os
 
@@ -22,6 +25,7 @@ from tests.gpu_harness import Dev, compare, note, values
 pytestmark = pytest.mark.gpu
 
 KS, VS = 0.0625, 0.0390625
+QS = 0.015625  # q_scale of the fp8-product runs (|q| / QS stays well inside 448 for these inputs)
 
 
 @pytest.fixture(autouse=True)
@@ -36,12 +40,14 @@ def _no_split_override():
 class Dev8(Dev):
     """Device copies of an fp8-cache case (uint8 pools) and its descriptor."""
 
-    def __init__(self, case, rope=None):
+    def __init__(self, case, rope=None, q8=False):
         super().__init__(case)
         self.k_pool = torch.from_numpy(case.k_pool).cuda()
         self.v_pool = torch.from_numpy(case.v_pool).cuda()
         self.desc.kv_dtype = csr.CSR_KV_FP8_E4M3
         self.desc.k_scale, self.desc.v_scale = KS, VS
+        if q8:
+            self.desc.q_scale = QS
         if rope is not None:
             self.desc.rope_style, self.desc.rope_dim, self.desc.rope_theta = rope
 
@@ -51,11 +57,11 @@ def fp8_case(label, cfg_id, **kw):
                              cfg_id=cfg_id)
 
 
-def oracle8(case, rows, rope=None, prefill=False):
+def oracle8(case, rows, rope=None, prefill=False, q8=False):
     out, lse, _ = oracle.attention(oracle.BF16, case.q, case.k_new, case.v_new, case.k_pool, case.v_pool,
                                    case.block_table, case.bt_stride, case.cu_seqlens_q,
                                    None if prefill else case.cache_len, rows, case.num_q_heads, case.num_kv_heads,
-                                   case.head_dim, case.page_size, rope=rope, fp8=(KS, VS))
+                                   case.head_dim, case.page_size, rope=rope, fp8=(KS, VS), q_fp8=QS if q8 else None)
     return out, lse
 
 
@@ -98,20 +104,21 @@ SMALL = [
 ]
 
 
+@pytest.mark.parametrize("q8", [False, True], ids=["bf16_scores", "fp8_scores"])
 @pytest.mark.parametrize("label,kw", SMALL, ids=[s[0] for s in SMALL])
 @pytest.mark.parametrize("nsplit", [None, 3])
-def test_fp8_extend_append_all_rows(label, kw, nsplit):
+def test_fp8_extend_append_all_rows(label, kw, nsplit, q8):
     if nsplit:
         os.environ["CSR_NSPLIT"] = str(nsplit)
     case = fp8_case(label, 600, **kw)
-    note(f"fp8 {label} nsplit={nsplit} L={case.cache_len.tolist()} n={case.seqlen_q.tolist()}: "
+    note(f"fp8 {label} nsplit={nsplit} q8={q8} L={case.cache_len.tolist()} n={case.seqlen_q.tolist()}: "
          "csr_extend_attention(APPEND)")
-    dev = Dev8(case)
+    dev = Dev8(case, q8=q8)
     out, lse = dev.extend(append=True)
     torch.cuda.synchronize()
     rows = np.arange(case.total_q, dtype=np.int32)
-    ref, ref_lse = oracle8(case, rows)
-    compare(case, out, lse, rows, ref, ref_lse, f"fp8/{label}/split={nsplit}")
+    ref, ref_lse = oracle8(case, rows, q8=q8)
+    compare(case, out, lse, rows, ref, ref_lse, f"fp8/{label}/split={nsplit}/q8={q8}")
     check_pool8(case, dev, case.cache_len)
 
 
@@ -125,34 +132,36 @@ def test_fp8_kv_append_alone():
     check_pool8(case, dev, case.cache_len)
 
 
+@pytest.mark.parametrize("q8", [False, True], ids=["bf16_scores", "fp8_scores"])
 @pytest.mark.parametrize("n", [[90], [1, 2, 1]], ids=["chunk90", "decode"])
 @pytest.mark.parametrize("style", [csr.CSR_ROPE_NEOX, csr.CSR_ROPE_INTERLEAVED])
-def test_fp8_with_rope(style, n):
+def test_fp8_with_rope(style, n, q8):
     L = [3000] if len(n) == 1 else [3000, 64, 777]
     case = fp8_case("rope8", 602, num_q_heads=16, num_kv_heads=2, cache_len=L, seqlen_q=n, page_size=16,
                     scale=0.5, interleave=len(n) > 1)
     rope = (style, 0, 1e6)
-    note(f"fp8 + rope style {style}, L={L} n={n}: csr_extend_attention(APPEND)")
-    dev = Dev8(case, rope)
+    note(f"fp8 + rope style {style}, L={L} n={n} q8={q8}: csr_extend_attention(APPEND)")
+    dev = Dev8(case, rope, q8=q8)
     out, lse = dev.extend(append=True)
     torch.cuda.synchronize()
     rows = np.arange(case.total_q, dtype=np.int32)
-    ref, ref_lse = oracle8(case, rows, rope=rope)
+    ref, ref_lse = oracle8(case, rows, rope=rope, q8=q8)
     compare(case, out, lse, rows, ref, ref_lse, f"fp8/rope{style}")
     check_pool8(case, dev, case.cache_len, rope=rope)
 
 
+@pytest.mark.parametrize("q8", [False, True], ids=["bf16_scores", "fp8_scores"])
 @pytest.mark.parametrize("n", [512, 1])
-def test_fp8_c3_120k_prefix(n):
+def test_fp8_c3_120k_prefix(n, q8):
     base = dg.config(f"c3_{n}")
     case = dg.with_fp8_pools(base, cfg_id=603)
-    note(f"fp8 c3 L=122880 n={n}: csr_extend_attention(APPEND)")
-    dev = Dev8(case)
+    note(f"fp8 c3 L=122880 n={n} q8={q8}: csr_extend_attention(APPEND)")
+    dev = Dev8(case, q8=q8)
     out, lse = dev.extend(append=True)
     torch.cuda.synchronize()
     rows = dg.sample_rows(case, 64, cfg_id=3)
-    ref, ref_lse = oracle8(case, rows)
-    compare(case, out, lse, rows, ref, ref_lse, f"fp8/c3_{n}")
+    ref, ref_lse = oracle8(case, rows, q8=q8)
+    compare(case, out, lse, rows, ref, ref_lse, f"fp8/c3_{n}/q8={q8}")
     check_pool8(case, dev, case.cache_len)
 
 
@@ -184,14 +193,15 @@ def test_fp8_chunk_split_on_device():
     assert np.abs(lse_b.cpu().numpy() - lse_one.cpu().numpy()[n1:]).max() < 1e-4
 
 
-def test_fp8_prefill_writes_the_quantised_cache():
+@pytest.mark.parametrize("q8", [False, True], ids=["bf16_scores", "fp8_scores"])
+def test_fp8_prefill_writes_the_quantised_cache(q8):
     case = fp8_case("pf8", 605, num_q_heads=16, num_kv_heads=2, cache_len=[0], seqlen_q=[2600], page_size=16,
                     scale=0.5)
-    note("fp8 csr_prefill with cache write")
-    dev = Dev8(case)
+    note(f"fp8 csr_prefill with cache write, q8={q8}")
+    dev = Dev8(case, q8=q8)
     out, lse = dev.prefill(write_cache=True)
     torch.cuda.synchronize()
     rows = dg.sample_rows(case, 48, cfg_id=6)
-    ref, ref_lse = oracle8(case, rows, prefill=True)
+    ref, ref_lse = oracle8(case, rows, prefill=True, q8=q8)
     compare(case, out, lse, rows, ref, ref_lse, "fp8/prefill")
     check_pool8(case, dev, None)
