@@ -194,7 +194,11 @@ csr_status make_plan(const csr_attn_desc* d, int batch, int total_q, int max_q, 
     const int cus = device_cus() * (p.four_waves ? 2 : 1);  // resident workgroups
     if (base > 0 && base < cus) {
       nsplit = (int)((cus + base - 1) / base);
-      const int cap = ntiles / 8 > 1 ? ntiles / 8 : 1;  // keep >= 8 key tiles per split
+      // bf16: keep >= 8 key tiles per split (its 4-stage DMA pipeline takes
+      // 3 tiles to fill); the fp32 kernel stages one tile ahead and splits
+      // down to a tile per split
+      const int min_tiles = d->dtype == CSR_BF16 ? 8 : 1;
+      const int cap = ntiles / min_tiles > 1 ? ntiles / min_tiles : 1;
       if (nsplit > cap) nsplit = cap;
     }
   }
