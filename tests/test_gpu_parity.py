@@ -55,6 +55,12 @@ SMALL = [
                           seqlen_q=[50, 77], page_size=128, scale=0.5, interleave=True)),
     ("bf16_page1024_max", dict(dtype=dg.BF16, num_q_heads=8, num_kv_heads=1, head_dim=64, cache_len=[3000],
                                seqlen_q=[41], page_size=1024, scale=0.5)),
+    # fp32 splits down to one key tile per split: 256 splits of a 20K prefix, merged by the
+    # one-workgroup-per-row merge (fp32 output)
+    ("f32_decode_long", dict(dtype=dg.F32, num_q_heads=4, num_kv_heads=1, head_dim=64, cache_len=[20000],
+                             seqlen_q=[1], page_size=16)),
+    ("f32_d128_long_ragged", dict(dtype=dg.F32, num_q_heads=8, num_kv_heads=2, head_dim=128, cache_len=[9000, 0, 3],
+                                  seqlen_q=[2, 5, 70], page_size=16, interleave=True)),
 ]
 
 
