@@ -14,7 +14,7 @@ import torch
 
 from paper_2605_07325_amd import csr
 from paper_2605_07325_amd import datagen as dg
-from tests.gpu_harness import Dev, note
+from tests.gpu_harness import Dev, compare, note, oracle_rows
 
 pytestmark = pytest.mark.gpu
 
@@ -30,21 +30,17 @@ def _restore_env():
         os.environ["CSR_NSPLIT"] = saved
 
 
-@pytest.mark.parametrize("nsplit", [1, 3])
-def test_work_order_is_a_longest_first_permutation(nsplit):
-    os.environ["CSR_NSPLIT"] = str(nsplit)
-    g = np.random.default_rng(17)
-    L = g.integers(0, 20000, size=7)
-    n = g.integers(9, 700, size=7)
-    n[2] = 700
-    case = dg.make_case("plan", dtype=dg.BF16, num_q_heads=64, num_kv_heads=4, head_dim=128, cache_len=L.tolist(),
-                        seqlen_q=n.tolist(), page_size=16, scale=0.5, seed=4, cfg_id=320, interleave=True)
-    note(f"work order: L={L.tolist()} n={n.tolist()} nsplit={nsplit}")
-    dev = Dev(case)
+def subgroup_rows(batch, hkv, mtiles):
+    """Row tiles per subgroup: 4, more when batch * Hkv * mtiles exceeds 3072."""
+    return max(4, -(-batch * hkv * mtiles // 768))
+
+
+def check_order(case, dev, nsplit, L, n):
+    """Runs the call, reads the order back and checks it; returns the output and LSE."""
     B, Hkv, G = case.batch, case.num_kv_heads, case.num_q_heads // case.num_kv_heads
     ws_bytes = csr.extend_workspace_size(dev.desc, B, case.total_q, case.max_seqlen_q, case.max_cache_len)
     ws = torch.zeros(ws_bytes, dtype=torch.uint8, device="cuda")
-    dev.extend(workspace=ws)
+    out, lse = dev.extend(workspace=ws)
     torch.cuda.synchronize()
     mtiles = math.ceil(case.max_seqlen_q * G / BM)
     units = B * Hkv * mtiles * nsplit
@@ -68,7 +64,8 @@ def test_work_order_is_a_longest_first_permutation(nsplit):
     got = order[order >= 0]
     assert len(got) == len(set(got.tolist())), "a unit is scheduled twice"
     assert set(got.tolist()) == active, "scheduled units differ from the active units"
-    spread = math.ceil(4 * BM / G / 64 / nsplit) + 1  # key tiles between the row tiles of one subgroup
+    K = subgroup_rows(B, Hkv, mtiles)
+    spread = math.ceil(K * BM / G / 64 / nsplit) + 1  # key tiles between the row tiles of one subgroup
     loads = []
     for x in range(8):
         q = [length(int(u)) for u in order[:, x] if u >= 0]
@@ -78,3 +75,40 @@ def test_work_order_is_a_longest_first_permutation(nsplit):
     note(f"work order ok: {len(got)} units, XCD loads {loads}")
     longest = max(length(u) for u in active)
     assert max(loads) <= sum(loads) / 8 + 8 * longest, "XCD loads far from balanced"
+    return out, lse
+
+
+@pytest.mark.parametrize("nsplit", [1, 3])
+def test_work_order_is_a_longest_first_permutation(nsplit):
+    os.environ["CSR_NSPLIT"] = str(nsplit)
+    g = np.random.default_rng(17)
+    L = g.integers(0, 20000, size=7)
+    n = g.integers(9, 700, size=7)
+    n[2] = 700
+    case = dg.make_case("plan", dtype=dg.BF16, num_q_heads=64, num_kv_heads=4, head_dim=128, cache_len=L.tolist(),
+                        seqlen_q=n.tolist(), page_size=16, scale=0.5, seed=4, cfg_id=320, interleave=True)
+    note(f"work order: L={L.tolist()} n={n.tolist()} nsplit={nsplit}")
+    check_order(case, Dev(case), nsplit, L, n)
+
+
+def test_work_order_at_the_group_limit_with_wider_subgroups():
+    """256 sequences x 4 kv heads = 1024 groups (the most one plan takes) of up to 7 row
+    tiles: 10 row tiles per subgroup; the order is checked as above and the outputs of
+    five sequences on every row against the oracle."""
+    os.environ["CSR_NSPLIT"] = "1"
+    g = np.random.default_rng(23)
+    B = 256
+    L = g.integers(0, 400, size=B)
+    n = g.integers(9, 112, size=B)
+    n[5] = 112
+    L[7] = 0
+    case = dg.make_case("plan1024", dtype=dg.BF16, num_q_heads=64, num_kv_heads=4, head_dim=128,
+                        cache_len=L.tolist(), seqlen_q=n.tolist(), page_size=16, scale=0.5, seed=4, cfg_id=321,
+                        interleave=True)
+    assert subgroup_rows(B, 4, math.ceil(112 * 16 / BM)) == 10
+    note(f"work order at 1024 groups: {B} sequences, n {int(n.min())}..{int(n.max())}, L {int(L.min())}..{int(L.max())}")
+    out, lse = check_order(case, Dev(case), 1, L, n)
+    cu = np.concatenate([[0], np.cumsum(n)])
+    rows = np.concatenate([np.arange(cu[b], cu[b + 1]) for b in (0, 5, 7, 128, B - 1)]).astype(np.int32)
+    ref, ref_lse = oracle_rows(case, rows)
+    compare(case, out, lse, rows, ref, ref_lse, "plan1024")
