@@ -65,6 +65,14 @@ constexpr int NTHREADS = 256;  // 4 waves
 constexpr int NWAVES = 4;
 constexpr float LN2 = 0.693147180559945309f;
 
+// Key rows one page lookup of the bf16-Q kernel covers (a run of one or two
+// 1 KB DMA blocks of one wave); the scalar page path needs pages at least this long.
+constexpr int dma_rows_per_lookup(int d, bool kv8, int nw, bool dma_upper) {
+  const int rowb = d * (kv8 ? 1 : 2);
+  const int ndma = KT * rowb / ((dma_upper ? nw / 2 : nw) * 1024);
+  return (ndma >= 2 ? 2 : 1) * (1024 / rowb);
+}
+
 // XOR swizzle of the 16-byte chunk index within a key row (NCH chunks per row).
 template <int NCH>
 __device__ __forceinline__ int swz(int row) {
@@ -122,6 +130,31 @@ __device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
 }
 
 __device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
+
+// LDS DMA (global_load_lds_dwordx4: 16 bytes per lane, 1 KB per wave) written
+// as inline assembly, so that the compiler neither merges the address paths
+// nor waits for these loads before unrelated LDS reads; every wait on them is
+// explicit.  M0 holds the LDS address; the instruction offset moves the LDS
+// and the global address alike, so run member i (LDS m0 + 1024 i) takes a
+// per-lane offset that already carries -1024 i.
+template <int N>
+__device__ __forceinline__ void dma_sbase(const char* base, uint32_t m0, const uint32_t* voff) {
+  static_assert(N == 1 || N == 2, "runs of one or two DMA blocks");
+  if constexpr (N == 1)
+    asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %1, %2"
+                 :
+                 : "s"(m0), "v"(voff[0]), "s"(base)
+                 : "memory");
+  else
+    asm volatile(
+        "s_mov_b32 m0, %0\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %1, %3\n\tglobal_load_lds_dwordx4 %2, %3 offset:1024"
+        :
+        : "s"(m0), "v"(voff[0]), "v"(voff[1]), "s"(base)
+        : "memory");
+}
+__device__ __forceinline__ void dma_vaddr(const char* src, uint32_t m0) {
+  asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %1, off" : : "s"(m0), "v"(src) : "memory");
+}
 
 // Everything a workgroup needs about its unit.
 struct Unit {
@@ -280,7 +313,12 @@ __global__ void __launch_bounds__(NW * 64, 8 / NW) attn_bf16_kernel(const AttnAr
   constexpr int DW = DMA_UPPER ? NW / 2 : NW;  // waves that issue the K/V DMA
   constexpr int NDMA = TILEB / (DW * 1024);    // DMA instructions per issuing wave per tensor tile
   static_assert(NDMA >= 1, "a tile must give every wave at least one DMA block");
-  constexpr int NH = (NDMA + 1) / 2;           // blocks issued in a tile's first step
+  constexpr int PB = NDMA >= 2 ? 2 : 1;        // consecutive blocks per run (one page, one M0)
+  constexpr int PG = SCALAR_PAGES ? PB : 1;    // blocks per page lookup
+  constexpr int NPG = NDMA / PG;               // page lookups per issuing wave per tile
+  constexpr int NG0 = (NPG + 1) / 2;           // lookup groups issued in a tile's first step
+  static_assert(!SCALAR_PAGES || PB * ROWS_PER_KB == dma_rows_per_lookup(D, KV8, NW, DMA_UPPER),
+                "scalar page lookups cover the rows the launcher checks against the page size");
   constexpr int ST = 4;                      // ring stages (K and V each)
   constexpr float THRESH = 8.f;              // lazy-rescale threshold (log2 units)
   __shared__ __attribute__((aligned(1024))) char lds[2 * ST * TILEB];
@@ -338,84 +376,101 @@ __global__ void __launch_bounds__(NW * 64, 8 / NW) attn_bf16_kernel(const AttnAr
       for (int ds = 0; ds < DS; ++ds)
         qf[ds] = valid ? *reinterpret_cast<const u32x4*>(qrow + ds * 32) : u32x4{0, 0, 0, 0};
     }
+    // Take delivery of q here, on every path: the K/V DMA below is invisible
+    // to the compiler, which would otherwise wait for "the q loads" with a
+    // vmcnt(0) inside the key loop, i.e. for every DMA in flight.
+#pragma unroll
+    for (int x = 0; x < NQF; ++x) asm volatile("" : "+v"(qf[x]));
   }
 
-  // ---- DMA: lane's key row within the tile for block j, and its byte offset inside a token row.
+  // ---- DMA.  Wave dw loads the 1 KB blocks blk(j) of every K and V tile, j < NDMA: runs of PB
+  // consecutive blocks (PB * ROWS_PER_KB consecutive key rows), so that with pages of at least
+  // that many keys one page lookup serves a run and one LDS address (M0) with instruction
+  // offsets 0 / 1024 serves its DMAs.  Lane's key row within the tile for block j, and its byte
+  // offset inside a token row:
+  auto blk = [&](int j) { return ((j / PB) * DW + dw) * PB + (j % PB); };
   int drow[NDMA], dchunk[NDMA];
   // Byte offsets of the lane's row inside a page (pool tiles) and inside the
   // chunk's K/V rows (chunk tiles): with 64-key tiles aligned to 64, a page of
   // P <= 64 keys starts the lane's in-page index at drow & (P-1); for P > 64
-  // the tile start inside the page is a scalar added separately.
-  int pool_off[NDMA], new_off[NDMA];
+  // the tile start inside the page is a scalar added separately.  The _v
+  // copies carry -1024 (j % PB): the instruction offset of the run's j-th DMA
+  // moves the global address by as much as the LDS one.
+  uint32_t pool_off[NDMA], new_off[NDMA], pool_v[NDMA], new_v[NDMA];
   const int in_page_mask = min((1 << a.log2P) - 1, KT - 1);
 #pragma unroll
   for (int j = 0; j < NDMA; ++j) {
-    drow[j] = (j * DW + dw) * ROWS_PER_KB + lane / NCH;
+    drow[j] = blk(j) * ROWS_PER_KB + lane / NCH;
     dchunk[j] = u.g * ROWB + (chunk_of_slot<NCH, KV8>(drow[j], lane % NCH) << 4);
     pool_off[j] = (drow[j] & in_page_mask) * (a.Hkv * ROWB) + dchunk[j];
     new_off[j] = drow[j] * (a.Hkv * ROWB) + dchunk[j];
+    pool_v[j] = pool_off[j] - 1024u * (j % PB);
+    new_v[j] = new_off[j] - 1024u * (j % PB);
   }
   // Byte offset, from the pool base, of the 64-key-aligned stretch of the page
-  // that holds DMA block j of `tile` (wave-uniform in scalar mode; per lane
-  // otherwise; unused for chunk keys).  Page ids outside [0, num_pages) read
-  // page 0 instead, so a bad table cannot send a load out of bounds.
+  // that holds lookup group g of `tile` (PG blocks; wave-uniform in scalar
+  // mode, per lane otherwise; unused for chunk keys).  Page ids outside
+  // [0, num_pages) read page 0 instead, so a bad table cannot send a load out
+  // of bounds.
   const int64_t page_bytes = (int64_t)kv_stride << log2P;
-  auto block_key = [&](int tile, int j) -> int {
+  auto block_key = [&](int tile, int g) -> int {
     if constexpr (SCALAR_PAGES)
-      return min(tile * KT + (j * DW + dw) * ROWS_PER_KB, last_key);
+      return min(tile * KT + blk(g * PB) * ROWS_PER_KB, last_key);
     else
-      return min(tile * KT + drow[j], last_key);
+      return min(tile * KT + drow[g], last_key);
   };
   // Split in two so that the block-table load can be issued well before the
   // offset is needed: page_id loads, page_off does the arithmetic.
-  auto page_id = [&](int tile, int j) -> int {
-    const int t = block_key(tile, j);
+  auto page_id = [&](int tile, int g) -> int {
+    const int t = block_key(tile, g);
     if (t >= u.L) return 0;
     const int pidx = t >> log2P;
     return bt ? bt[pidx] : bt_base + pidx;
   };
-  auto page_off = [&](int tile, int j, int pg) -> int64_t {
-    const int t = block_key(tile, j);
-    pg = (pg >= 0 && pg < num_pages) ? pg : 0;
+  auto page_off = [&](int tile, int g, int pg) -> int64_t {
+    const int t = block_key(tile, g);
+    pg = (uint32_t)pg < (uint32_t)num_pages ? pg : 0;
     return (int64_t)(uint32_t)pg * page_bytes + (int64_t)((t & Pmask & ~(KT - 1)) * kv_stride);
   };
-  auto page_of = [&](int tile, int j) -> int64_t { return page_off(tile, j, page_id(tile, j)); };
-  auto dma = [&](const char* src, char* dst, int j) {
-    __builtin_amdgcn_global_load_lds((const __attribute__((address_space(1))) void*)src,
-                                     (__attribute__((address_space(3))) void*)(dst + (j * DW + dw) * 1024), 16, 0, 0);
+  auto page_of = [&](int tile, int g) -> int64_t { return page_off(tile, g, page_id(tile, g)); };
+  auto lds_addr = [](const char* p) -> uint32_t {
+    return (uint32_t)(size_t)((const __attribute__((address_space(3))) char*)p);
   };
-  // DMA block j of a K or V tile into `dst`.  A tile wholly inside the prefix
-  // or wholly inside the chunk takes a scalar base plus the lane's constant
-  // 32-bit offset; a tile straddling L or ending the key range selects per lane.
-  // (The empty asm markers keep the three loads apart: merged, their address
-  // would become a per-lane 64-bit value on every path.)
-  auto issue_block = [&](int tile, int j, int64_t pgoff, char* dst, const char* pool_base, const char* new_base) {
+  // The DMA of lookup group g of a K or V tile into `dst`.  A tile wholly
+  // inside the prefix or wholly inside the chunk takes a scalar base plus the
+  // lanes' constant 32-bit offsets; a tile straddling L or ending the key
+  // range selects per lane.
+  auto issue_group = [&](int tile, int g, int64_t pgoff, char* dst, const char* pool_base, const char* new_base) {
     const int t0 = tile * KT;
-    const uint32_t po = pool_off[j], no = new_off[j];
-    const int dr = drow[j], dc = dchunk[j];
-    if (t0 + KT - 1 < u.L) {
-      // The opaque scalar base keeps the sum in SGPRs: otherwise the
-      // loop-invariant pool_base + po is hoisted into a 64-bit VGPR pair.
-      const char* base = pool_base + pgoff;
-      if constexpr (SCALAR_PAGES) asm("" : "+s"(base));
-      dma(base + po, dst, j);
-      asm volatile("; dma prefix tile");
-    } else if (t0 >= u.L && t0 + KT - 1 <= last_key) {
-      const char* base = new_base + (int64_t)(u.cuq + t0 - u.L) * kv_stride;
-      asm("" : "+s"(base));
-      dma(base + no, dst, j);
-      asm volatile("; dma chunk tile");
+    if constexpr (SCALAR_PAGES) {
+      const uint32_t m0 = lds_addr(dst) + blk(g * PB) * 1024;
+      if (t0 + KT - 1 < u.L) {
+        dma_sbase<PB>(pool_base + pgoff, m0, &pool_v[g * PB]);
+        return;
+      }
+      if (t0 >= u.L && t0 + KT - 1 <= last_key) {
+        dma_sbase<PB>(new_base + (int64_t)(u.cuq + t0 - u.L) * kv_stride, m0, &new_v[g * PB]);
+        return;
+      }
+#pragma unroll
+      for (int i = 0; i < PB; ++i) {
+        const int j = g * PB + i;
+        const int t = min(t0 + drow[j], last_key);
+        const char* src = t < u.L ? pool_base + pgoff + pool_off[j]
+                                  : new_base + (int64_t)(u.cuq + t - u.L) * kv_stride + dchunk[j];
+        dma_vaddr(src, m0 + 1024u * i);
+      }
     } else {
-      const int t = min(t0 + dr, last_key);
-      const char* src = t < u.L ? pool_base + pgoff + po : new_base + (int64_t)(u.cuq + t - u.L) * kv_stride + dc;
-      dma(src, dst, j);
-      asm volatile("; dma mixed tile");
+      const int t = min(t0 + drow[g], last_key);
+      const char* src = t < u.L ? pool_base + pgoff + pool_off[g]
+                                : new_base + (int64_t)(u.cuq + t - u.L) * kv_stride + dchunk[g];
+      dma_vaddr(src, lds_addr(dst) + blk(g) * 1024);
     }
   };
   auto issue = [&](int tile, const int64_t* pg, char* dst, const char* pool_base, const char* new_base) {
     if (!dma_wave) return;
 #pragma unroll
-    for (int j = 0; j < NDMA; ++j) issue_block(tile, j, pg[j], dst, pool_base, new_base);
+    for (int g = 0; g < NPG; ++g) issue_group(tile, g, pg[g], dst, pool_base, new_base);
   };
   // K ring first: its stage and block offsets then fit the 16-bit DS offset
   // field; the V ring's base is folded into the per-lane V read addresses.
@@ -688,21 +743,21 @@ __global__ void __launch_bounds__(NW * 64, 8 / NW) attn_bf16_kernel(const AttnAr
     // last one and land in a stage nobody reads again), so "all but the
     // previous tile's loads" is the constant vmcnt(2*NDMA).
     auto clampt = [&](int t) { return min(t, main_end - 1); };
-    int64_t pgn[NDMA];  // page offsets of tile tb+k+3, issued at tile k
-    int pgi[NDMA];      // their raw page ids, loaded half a tile earlier
+    int64_t pgn[NPG];  // page offsets of tile tb+k+3, issued at tile k
+    int pgi[NPG];      // their raw page ids, loaded half a tile earlier
     {
-      int64_t pg[NDMA];
+      int64_t pg[NPG];
       if (dma_wave) {
 #pragma unroll
         for (int i = 0; i < 3; ++i) {
 #pragma unroll
-          for (int j = 0; j < NDMA; ++j) pg[j] = page_of(clampt(u.tb + i), j);
+          for (int g = 0; g < NPG; ++g) pg[g] = page_of(clampt(u.tb + i), g);
           issue(clampt(u.tb + i), pg, kring + i * TILEB, kpool, knew);
           issue(clampt(u.tb + i), pg, vring + i * TILEB, vpool, vnew);
         }
       }
 #pragma unroll
-      for (int j = 0; j < NDMA; ++j) pgi[j] = dma_wave ? page_id(clampt(u.tb + 3), j) : 0;
+      for (int g = 0; g < NPG; ++g) pgi[g] = dma_wave ? page_id(clampt(u.tb + 3), g) : 0;
     }
     asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
     __syncthreads();
@@ -727,7 +782,7 @@ __global__ void __launch_bounds__(NW * 64, 8 / NW) attn_bf16_kernel(const AttnAr
       const int nt = clampt(u.tb + k + 3);
       if (dma_wave) {
 #pragma unroll
-        for (int j = 0; j < NDMA; ++j) pgn[j] = page_off(nt, j, pgi[j]);
+        for (int g = 0; g < NPG; ++g) pgn[g] = page_off(nt, g, pgi[g]);
       }
       char* kdst = kring + ((S + 3) % ST) * TILEB;
       char* vdst = vring + ((S + 3) % ST) * TILEB;
@@ -735,24 +790,24 @@ __global__ void __launch_bounds__(NW * 64, 8 / NW) attn_bf16_kernel(const AttnAr
       auto kd0 = [&] {
         if (!dma_wave) return;
 #pragma unroll
-        for (int j = 0; j < NH; ++j) issue_block(nt, j, pgn[j], kdst, kpool, knew);
+        for (int g = 0; g < NG0; ++g) issue_group(nt, g, pgn[g], kdst, kpool, knew);
       };
       auto kd1 = [&] {
         if (!dma_wave) return;
 #pragma unroll
-        for (int j = NH; j < NDMA; ++j) issue_block(nt, j, pgn[j], kdst, kpool, knew);
+        for (int g = NG0; g < NPG; ++g) issue_group(nt, g, pgn[g], kdst, kpool, knew);
       };
       auto vd0 = [&] {
         if (!dma_wave) return;
 #pragma unroll
-        for (int j = 0; j < NH; ++j) issue_block(nt, j, pgn[j], vdst, vpool, vnew);
+        for (int g = 0; g < NG0; ++g) issue_group(nt, g, pgn[g], vdst, vpool, vnew);
       };
       auto vd1 = [&] {
         if (!dma_wave) return;
 #pragma unroll
-        for (int j = NH; j < NDMA; ++j) issue_block(nt, j, pgn[j], vdst, vpool, vnew);
+        for (int g = NG0; g < NPG; ++g) issue_group(nt, g, pgn[g], vdst, vpool, vnew);
 #pragma unroll
-        for (int j = 0; j < NDMA; ++j) pgi[j] = page_id(clampt(u.tb + k + 4), j);
+        for (int g = 0; g < NPG; ++g) pgi[g] = page_id(clampt(u.tb + k + 4), g);
       };
       // The two waves of a SIMD take turns at the higher issue priority, one
       // step each, so that neither lags the other into the tile barrier.
@@ -783,9 +838,9 @@ __global__ void __launch_bounds__(NW * 64, 8 / NW) attn_bf16_kernel(const AttnAr
 
   // ---- tail: tiles [main_end, te) with the causal mask, one tile at a time
   for (int it = max(main_end, u.tb); it < u.te; ++it) {
-    int64_t pg[NDMA];
+    int64_t pg[NPG];
 #pragma unroll
-    for (int j = 0; j < NDMA; ++j) pg[j] = dma_wave ? page_of(it, j) : 0;
+    for (int g = 0; g < NPG; ++g) pg[g] = dma_wave ? page_of(it, g) : 0;
     issue(it, pg, kring, kpool, knew);
     issue(it, pg, vring, vpool, vnew);
     asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
@@ -1000,15 +1055,20 @@ int attn_block_m(int dtype_bf16, int d, int four_waves) {
 
 namespace {
 
-// One bf16-Q kernel variant, with the DMA issued by every wave or by the upper half only.
-template <int D, bool SCALAR_PAGES, bool KV8, int NW, bool QK8 = false>
+// One bf16-Q kernel variant: the DMA issued by every wave or by the upper half
+// only, and the scalar page path when every page lookup run fits in a page.
+template <int D, bool KV8, int NW, bool QK8 = false>
 void launch_bf16(const AttnArgs& a, unsigned grid, hipStream_t stream) {
-  if (a.dma_upper)
-    hipLaunchKernelGGL((attn_bf16_kernel<D, SCALAR_PAGES, KV8, NW, true, QK8>), dim3(grid), dim3(NW * 64), 0, stream,
-                       a);
-  else
-    hipLaunchKernelGGL((attn_bf16_kernel<D, SCALAR_PAGES, KV8, NW, false, QK8>), dim3(grid), dim3(NW * 64), 0, stream,
-                       a);
+  const bool up = a.dma_upper != 0;
+  const bool sp = a.P >= dma_rows_per_lookup(D, KV8, NW, up);
+  const dim3 g(grid), b(NW * 64);
+  if (up) {
+    if (sp) hipLaunchKernelGGL((attn_bf16_kernel<D, true, KV8, NW, true, QK8>), g, b, 0, stream, a);
+    else hipLaunchKernelGGL((attn_bf16_kernel<D, false, KV8, NW, true, QK8>), g, b, 0, stream, a);
+  } else {
+    if (sp) hipLaunchKernelGGL((attn_bf16_kernel<D, true, KV8, NW, false, QK8>), g, b, 0, stream, a);
+    else hipLaunchKernelGGL((attn_bf16_kernel<D, false, KV8, NW, false, QK8>), g, b, 0, stream, a);
+  }
 }
 
 }  // namespace
@@ -1018,36 +1078,18 @@ hipError_t launch_attention(const AttnArgs& a, int dtype_bf16, hipStream_t strea
   unsigned grid = (unsigned)a.n_units;
   if (a.order) grid = 8u * (unsigned)a.order_slots;
   else if (a.xcd_remap) grid = (grid + 7u) & ~7u;
-  if (dtype_bf16 && a.kv_fp8 && a.four_waves) {
-    // fp8 rows, 4 waves: still 8 keys per 1 KB DMA block
-    if (a.qk8) {
-      if (a.P >= 8) launch_bf16<128, true, true, 4, true>(a, grid, stream);
-      else launch_bf16<128, false, true, 4, true>(a, grid, stream);
+  if (dtype_bf16 && a.kv_fp8) {
+    // fp8 rows (d = 128); 4-wave workgroups of 128 rows for short chunks
+    if (a.four_waves) {
+      if (a.qk8) launch_bf16<128, true, 4, true>(a, grid, stream);
+      else launch_bf16<128, true, 4>(a, grid, stream);
     } else {
-      if (a.P >= 8) launch_bf16<128, true, true, 4>(a, grid, stream);
-      else launch_bf16<128, false, true, 4>(a, grid, stream);
-    }
-  } else if (dtype_bf16 && a.kv_fp8) {
-    // fp8 rows: 8 keys per DMA block (more than 128 packed rows: every wave computes)
-    if (a.qk8) {
-      if (a.P >= 8)
-        hipLaunchKernelGGL((attn_bf16_kernel<128, true, true, 8, false, true>), dim3(grid), dim3(512), 0, stream, a);
-      else
-        hipLaunchKernelGGL((attn_bf16_kernel<128, false, true, 8, false, true>), dim3(grid), dim3(512), 0, stream, a);
-    } else {
-      if (a.P >= 8) hipLaunchKernelGGL((attn_bf16_kernel<128, true, true>), dim3(grid), dim3(512), 0, stream, a);
-      else hipLaunchKernelGGL((attn_bf16_kernel<128, false, true>), dim3(grid), dim3(512), 0, stream, a);
+      if (a.qk8) launch_bf16<128, true, 8, true>(a, grid, stream);
+      else launch_bf16<128, true, 8>(a, grid, stream);
     }
   } else if (dtype_bf16) {
-    // Scalar page-id loads need every DMA block (4 keys at d=128, 8 at d=64) inside one page.
-    const bool scalar_pages = a.P >= (a.d == 128 ? 4 : 8);
-    if (a.d == 128) {
-      if (scalar_pages) launch_bf16<128, true, false, 8>(a, grid, stream);
-      else launch_bf16<128, false, false, 8>(a, grid, stream);
-    } else {
-      if (scalar_pages) launch_bf16<64, true, false, 8>(a, grid, stream);
-      else launch_bf16<64, false, false, 8>(a, grid, stream);
-    }
+    if (a.d == 128) launch_bf16<128, false, 8>(a, grid, stream);
+    else launch_bf16<64, false, 8>(a, grid, stream);
   } else {
     if (a.d == 128) hipLaunchKernelGGL((attn_f32_kernel<128>), dim3(grid), dim3(NTHREADS), 0, stream, a);
     else hipLaunchKernelGGL((attn_f32_kernel<64>), dim3(grid), dim3(NTHREADS), 0, stream, a);
