@@ -222,6 +222,7 @@ def run_asr(args, torch, csr):
         if limit is not None:
             del rec
             torch.cuda.synchronize()
+            asr.destroy_streams(ps, ss)
             return None, None
         full = np.asarray(rec.latencies_ms())
         lat = full[skip:]
@@ -252,6 +253,7 @@ def run_asr(args, torch, csr):
             f"max {res['max_ms']:.3f} ms" + (f"; events {res.get('events')}" if mode != "steady" else ""))
         del rec
         torch.cuda.synchronize()
+        asr.destroy_streams(ps, ss)
         torch.cuda.empty_cache()
         return res, lat
 

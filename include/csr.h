@@ -67,23 +67,21 @@
  * Streams: every call enqueues its kernels on `stream` (a hipStream_t passed
  * as void*, NULL = the default stream) and returns without waiting.
  *
- * Errors: arguments are validated on the host before any HIP runtime call;
- * a failed check returns CSR_E_INVAL / CSR_E_UNSUPPORTED / CSR_E_WORKSPACE and
- * enqueues nothing.  A launch error returns CSR_E_HIP.  csr_last_error() gives
- * a thread-local description of the last failure.  Block-table contents are a
- * caller contract: every page a call touches must be a valid id in
- * [0, num_pages); ids outside that range are never dereferenced (attention
- * reads some other in-bounds key row in its place, the append row is dropped)
- * so a bad table cannot fault the GPU, but the result is then unspecified.
+ * Errors: every argument is validated on the host before any work is
+ * enqueued; a failed check returns CSR_E_INVAL / CSR_E_UNSUPPORTED /
+ * CSR_E_WORKSPACE and enqueues nothing.  The only HIP runtime calls made
+ * before the checks end are two queries the launch plan (and with it the
+ * workspace size) depends on: hipGetDevice, and on the first call for a
+ * device its CU count (cached for the process).  A launch error returns
+ * CSR_E_HIP.  csr_last_error() gives a thread-local description of the last
+ * failure.  Block-table contents are a caller contract: every page a call
+ * touches must be a valid id in [0, num_pages); ids outside that range are
+ * never dereferenced (attention reads some other in-bounds key row in its
+ * place, the append row is dropped) so a bad table cannot fault the GPU, but
+ * the result is then unspecified.
  *
- * Environment overrides (testing and A/B measurement only; read at every
- * call, so a workspace query and the call it sizes must see the same values):
- *   CSR_NSPLIT=k      split the key range of every unit into k parts (changes
- *                     the summation order: results move within rounding)
- *   CSR_ORDER=0       ragged batches run their units in index order instead of
- *                     the device-side longest-first order (identical results)
- *   CSR_DMA_UPPER=0   short chunks load K/V from every wave instead of only the
- *                     waves without rows (identical results)
+ * Nothing in the environment changes what a call computes; the plan can be
+ * steered only through csr_set_plan_overrides (testing and A/B measurement).
  */
 #ifndef CSR_H
 #define CSR_H
@@ -239,6 +237,22 @@ csr_status csr_prefill(const csr_attn_desc* desc, int32_t batch, const void* q, 
  * hook off.  Returns CSR_E_INVAL if exactly one of them is NULL.
  */
 csr_status csr_set_attention_events(void* begin_event, void* end_event);
+
+/*
+ * Testing and A/B measurement only: steer the launch plan of later
+ * csr_extend_attention / csr_prefill calls and workspace queries made on this
+ * thread (a workspace query and the call it sizes must see the same values).
+ *   nsplit          > 0: split the key range of every unit into nsplit parts
+ *                   (changes the summation order: results move within
+ *                   rounding); 0: the planner's choice
+ *   fixed_order     1: ragged batches run their units in index order instead
+ *                   of the device-side longest-first order (identical results)
+ *   dma_all_waves   1: short chunks load K/V from every wave instead of only
+ *                   the waves without rows (identical results)
+ * All zero restores the planner.  Returns CSR_E_INVAL for a negative nsplit or
+ * flags other than 0 and 1.
+ */
+csr_status csr_set_plan_overrides(int32_t nsplit, int32_t fixed_order, int32_t dma_all_waves);
 
 /* Static name of a status code. */
 const char* csr_status_string(csr_status status);

@@ -63,13 +63,23 @@ def xcd_spread_cus(per_xcd: int, num_cus: int = 256, num_xcds: int = 8) -> List[
 
 
 _hip = None
+_owned = set()  # raw handles of the CU-masked streams this module created and has not destroyed
 
 
-def cu_masked_stream(cu_ids: List[int], num_cus: int = 256) -> torch.cuda.ExternalStream:
-    """A HIP stream (default priority) whose kernels run only on ``cu_ids``."""
+def _hip_lib():
     global _hip
     if _hip is None:
         _hip = ctypes.CDLL("libamdhip64.so")
+        _hip.hipStreamDestroy.argtypes = [ctypes.c_void_p]
+    return _hip
+
+
+def cu_masked_stream(cu_ids: List[int], num_cus: int = 256) -> torch.cuda.ExternalStream:
+    """A HIP stream (default priority) whose kernels run only on ``cu_ids``.
+
+    The stream belongs to the caller, who ends it with ``destroy_streams``
+    once its work is done (torch's ExternalStream never destroys the handle)."""
+    _hip_lib()
     if not cu_ids:
         raise ValueError("empty CU set")
     words = [0] * ((num_cus + 31) // 32)
@@ -80,7 +90,24 @@ def cu_masked_stream(cu_ids: List[int], num_cus: int = 256) -> torch.cuda.Extern
     rc = _hip.hipExtStreamCreateWithCUMask(ctypes.byref(s), len(words), arr)
     if rc != 0:
         raise RuntimeError(f"hipExtStreamCreateWithCUMask failed ({rc})")
+    _owned.add(s.value)
     return torch.cuda.ExternalStream(s.value)
+
+
+def destroy_streams(*streams) -> None:
+    """Wait for and destroy the given streams that ``cu_masked_stream`` created
+    (others, e.g. torch's own streams, are left alone).  A process should end
+    none of them alive: a stream left to the runtime's exit-time teardown is
+    destroyed after tools hooked into the runtime (profilers) have shut down."""
+    for st in streams:
+        h = getattr(st, "cuda_stream", None)
+        if h is None or h not in _owned:
+            continue
+        st.synchronize()
+        rc = _hip_lib().hipStreamDestroy(ctypes.c_void_p(h))
+        _owned.discard(h)
+        if rc != 0:
+            raise RuntimeError(f"hipStreamDestroy failed ({rc})")
 
 
 class TokenTable:

@@ -7,6 +7,7 @@ built (``python -m paper_2605_07325_amd.build``); there is no fallback.
 """
 from __future__ import annotations
 
+import contextlib
 import ctypes
 import os
 from typing import Optional
@@ -24,7 +25,8 @@ CSR_KV_SAME, CSR_KV_FP8_E4M3 = 0, 1
 
 # Every function include/csr.h declares.
 EXPORTS = ("csr_kv_append", "csr_extend_workspace_size", "csr_extend_attention", "csr_prefill_workspace_size",
-           "csr_prefill", "csr_set_attention_events", "csr_status_string", "csr_last_error")
+           "csr_prefill", "csr_set_attention_events", "csr_set_plan_overrides", "csr_status_string",
+           "csr_last_error")
 
 
 class AttnDesc(ctypes.Structure):
@@ -64,6 +66,8 @@ def lib() -> ctypes.CDLL:
         L.csr_prefill.restype = ctypes.c_int
         L.csr_set_attention_events.argtypes = [p, p]
         L.csr_set_attention_events.restype = ctypes.c_int
+        L.csr_set_plan_overrides.argtypes = [i32, i32, i32]
+        L.csr_set_plan_overrides.restype = ctypes.c_int
         L.csr_status_string.argtypes = [ctypes.c_int]
         L.csr_status_string.restype = ctypes.c_char_p
         L.csr_last_error.argtypes = []
@@ -88,6 +92,21 @@ def set_attention_events(begin_event, end_event) -> None:
     """csr_set_attention_events: raw hipEvent_t handles (ints) or None to disable."""
     _check(lib().csr_set_attention_events(None if begin_event is None else ctypes.c_void_p(begin_event),
                                           None if end_event is None else ctypes.c_void_p(end_event)))
+
+
+def set_plan_overrides(nsplit: int = 0, fixed_order: bool = False, dma_all_waves: bool = False) -> None:
+    """csr_set_plan_overrides (testing and A/B measurement, this thread): all defaults restore the planner."""
+    _check(lib().csr_set_plan_overrides(int(nsplit), int(bool(fixed_order)), int(bool(dma_all_waves))))
+
+
+@contextlib.contextmanager
+def plan_overrides(nsplit: int = 0, fixed_order: bool = False, dma_all_waves: bool = False):
+    """Plan overrides for the calls inside the block; the planner's choice again afterwards."""
+    set_plan_overrides(nsplit, fixed_order, dma_all_waves)
+    try:
+        yield
+    finally:
+        set_plan_overrides()
 
 
 def make_desc(num_q_heads: int, num_kv_heads: int, head_dim: int, page_size: int = 16, dtype=torch.bfloat16,
@@ -115,8 +134,31 @@ def _stream(stream) -> ctypes.c_void_p:
     return ctypes.c_void_p(stream.cuda_stream if hasattr(stream, "cuda_stream") else int(stream))
 
 
-def _pages(pool: Optional[torch.Tensor]) -> int:
-    return 0 if pool is None else int(pool.shape[0])
+def _pages(desc: AttnDesc, pool: Optional[torch.Tensor]) -> int:
+    """num_pages of a [num_pages][P][Hkv][d] pool, after checking that the tensor has exactly that
+    layout: num_pages bounds every page id the kernels dereference, so a pool of another shape
+    (say flattened to slots) must not reach the library."""
+    if pool is None:
+        return 0
+    want = (desc.page_size, desc.num_kv_heads, desc.head_dim)
+    if pool.dim() != 4 or tuple(pool.shape[1:]) != want:
+        raise ValueError(f"pool must be [num_pages, {want[0]}, {want[1]}, {want[2]}], got {tuple(pool.shape)}")
+    if desc.kv_dtype == CSR_KV_FP8_E4M3:
+        dt = torch.uint8
+    else:
+        dt = torch.bfloat16 if desc.dtype == CSR_BF16 else torch.float32
+    if pool.dtype != dt:
+        raise ValueError(f"pool dtype {pool.dtype}, expected {dt}")
+    if not pool.is_contiguous() or not pool.is_cuda:
+        raise ValueError("pool must be a contiguous device tensor")
+    return int(pool.shape[0])
+
+
+def _pool_pages(desc: AttnDesc, k_pool: Optional[torch.Tensor], v_pool: Optional[torch.Tensor]) -> int:
+    n = _pages(desc, k_pool)
+    if (k_pool is None) != (v_pool is None) or _pages(desc, v_pool) != n:
+        raise ValueError("k_pool and v_pool must both be given, with the same shape, or both be None")
+    return n
 
 
 def kv_append(desc: AttnDesc, k_new, v_new, k_pool, v_pool, block_table, bt_stride: int, cu_seqlens_q,
@@ -124,7 +166,7 @@ def kv_append(desc: AttnDesc, k_new, v_new, k_pool, v_pool, block_table, bt_stri
     """csr_kv_append: copy chunk K/V rows to cache positions L_b + i."""
     batch = int(cu_seqlens_q.shape[0]) - 1
     _check(lib().csr_kv_append(ctypes.byref(desc), batch, _ptr(k_new), _ptr(v_new), _ptr(k_pool), _ptr(v_pool),
-                               _pages(k_pool), _ptr(block_table), bt_stride, _ptr(cu_seqlens_q), _ptr(cache_seqlens),
+                               _pool_pages(desc, k_pool, v_pool), _ptr(block_table), bt_stride, _ptr(cu_seqlens_q), _ptr(cache_seqlens),
                                int(k_new.shape[0]), _stream(stream)))
 
 
@@ -159,7 +201,7 @@ def extend_attention(desc: AttnDesc, q, k_new, v_new, k_pool, v_pool, block_tabl
     workspace = _workspace(ws_bytes, q.device, workspace)
     ws_cap = 0 if workspace is None else workspace.numel() * workspace.element_size()
     _check(lib().csr_extend_attention(
-        ctypes.byref(desc), batch, _ptr(q), _ptr(k_new), _ptr(v_new), _ptr(k_pool), _ptr(v_pool), _pages(k_pool),
+        ctypes.byref(desc), batch, _ptr(q), _ptr(k_new), _ptr(v_new), _ptr(k_pool), _ptr(v_pool), _pool_pages(desc, k_pool, v_pool),
         _ptr(block_table), bt_stride, _ptr(cu_seqlens_q), _ptr(cache_seqlens), total_q, max_seqlen_q, max_cache_len,
         CSR_APPEND if append else 0, _ptr(out), _ptr(lse), _ptr(workspace), ws_cap, _stream(stream)))
     return out, lse
@@ -178,7 +220,7 @@ def prefill(desc: AttnDesc, q, k, v, cu_seqlens, max_seqlen: int, k_pool=None, v
     workspace = _workspace(ws_bytes, q.device, workspace)
     ws_cap = 0 if workspace is None else workspace.numel() * workspace.element_size()
     _check(lib().csr_prefill(
-        ctypes.byref(desc), batch, _ptr(q), _ptr(k), _ptr(v), _ptr(k_pool), _ptr(v_pool), _pages(k_pool),
+        ctypes.byref(desc), batch, _ptr(q), _ptr(k), _ptr(v), _ptr(k_pool), _ptr(v_pool), _pool_pages(desc, k_pool, v_pool),
         _ptr(block_table), bt_stride, _ptr(cu_seqlens), total, max_seqlen, _ptr(out), _ptr(lse), _ptr(workspace),
         ws_cap, _stream(stream)))
     return out, lse

@@ -1,14 +1,16 @@
 // C ABI of libcsr (declared in include/csr.h): host-side validation, launch
 // planning and kernel launches on the caller's stream.
 //
-// Validation runs entirely on the host and precedes every HIP runtime call,
-// so malformed arguments are rejected without touching the device.
+// Argument validation runs entirely on the host before any work is enqueued:
+// the only runtime queries before the last check (the workspace size, which
+// depends on the plan) are hipGetDevice and, once per device, its CU count.
 #include <math.h>
 #include <stdarg.h>
 #include <stdint.h>
 #include <stdio.h>
 #include <stdlib.h>
 
+#include <atomic>
 #include <string>
 
 #include "../../include/csr.h"
@@ -18,6 +20,13 @@ namespace {
 
 thread_local std::string g_last_error;
 thread_local hipEvent_t g_ev_begin = nullptr, g_ev_end = nullptr;  // csr_set_attention_events
+// csr_set_plan_overrides (testing and A/B measurement): 0 = the planner's choice.
+struct PlanOverrides {
+  int nsplit = 0;         // > 0: key-range splits per unit
+  int fixed_order = 0;    // 1: ragged batches keep the index order of their units
+  int dma_all_waves = 0;  // 1: short chunks load K/V from every wave
+};
+thread_local PlanOverrides g_ovr;
 
 csr_status fail(csr_status st, const char* fmt, ...) __attribute__((format(printf, 2, 3)));
 csr_status fail(csr_status st, const char* fmt, ...) {
@@ -143,9 +152,8 @@ csr::RopeArgs rope_args(const csr_attn_desc* d, int batch, const void* q, const 
   a.log2P = ilog2(d->page_size);
   a.rdim = has_rope(d) ? (d->rope_dim ? d->rope_dim : d->head_dim) : 0;
   a.style = d->rope_style;
-  // Pair i turns by pos * theta^(-2i/r) radians: store that rate in half-turns.
-  for (int i = 0; i < 64; ++i)
-    a.half_turns[i] = i < a.rdim / 2 ? pow((double)d->rope_theta, -2.0 * i / a.rdim) / M_PI : 0.0;
+  // Pair i turns by pos * theta^(-2i/r) radians (theta: the descriptor's float, widened).
+  for (int i = 0; i < 64; ++i) a.inv_freq[i] = i < a.rdim / 2 ? pow((double)d->rope_theta, -2.0 * i / a.rdim) : 0.0;
   return a;
 }
 
@@ -159,13 +167,25 @@ struct Plan {
   size_t ws_o, ws_lse, ws_order_off, ws_bytes;
 };
 
+// CU count of the current device, queried once per device (256 on MI355X).
+constexpr int kMaxDevices = 64;
+std::atomic<int> g_cus[kMaxDevices];
 int device_cus() {
-  int dev = 0, cus = 0;
-  if (hipGetDevice(&dev) != hipSuccess) return 256;
-  if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || cus <= 0) {
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0) {
     (void)hipGetLastError();
     return 256;
   }
+  if (dev < kMaxDevices) {
+    const int c = g_cus[dev].load(std::memory_order_relaxed);
+    if (c > 0) return c;
+  }
+  int cus = 0;
+  if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || cus <= 0) {
+    (void)hipGetLastError();
+    cus = 256;
+  }
+  if (dev < kMaxDevices) g_cus[dev].store(cus, std::memory_order_relaxed);
   return cus;
 }
 
@@ -182,14 +202,12 @@ csr_status make_plan(const csr_attn_desc* d, int batch, int total_q, int max_q, 
   p.mtiles = (int)((rows + p.bm - 1) / p.bm);
   // Short chunks leave the upper half of the waves without rows: they then
   // issue all of the K/V DMA, off the computing waves' critical path.
-  const char* dup = getenv("CSR_DMA_UPPER");  // 0: every wave loads (A/B)
-  p.dma_upper = d->dtype == CSR_BF16 && rows <= p.bm / 2 && !(dup && atoi(dup) == 0) ? 1 : 0;
+  p.dma_upper = d->dtype == CSR_BF16 && rows <= p.bm / 2 && !g_ovr.dma_all_waves ? 1 : 0;
   const int64_t base = (int64_t)batch * d->num_kv_heads * p.mtiles;
   const int ntiles = (max_L + max_q + 63) / 64;
   int nsplit = 1;
-  const char* env = getenv("CSR_NSPLIT");  // tuning override
-  if (env && atoi(env) > 0) {
-    nsplit = atoi(env);
+  if (g_ovr.nsplit > 0) {
+    nsplit = g_ovr.nsplit;
   } else {
     const int cus = device_cus() * (p.four_waves ? 2 : 1);  // resident workgroups
     if (base > 0 && base < cus) {
@@ -224,9 +242,7 @@ csr_status make_plan(const csr_attn_desc* d, int batch, int total_q, int max_q, 
   // with room.
   p.order_slots = 0;
   p.ws_order_off = 0;
-  const char* ord = getenv("CSR_ORDER");  // 0: keep the fixed order (A/B)
-  const bool want_order = !(ord && atoi(ord) == 0);
-  if (want_order && batch > 1 && (int64_t)batch * d->num_kv_heads <= 1024) {
+  if (!g_ovr.fixed_order && batch > 1 && (int64_t)batch * d->num_kv_heads <= 1024) {
     p.order_slots = (int)((units + 7) / 8 + (int64_t)p.mtiles * nsplit);
     p.ws_order_off = align256(p.ws_bytes);
     p.ws_bytes = p.ws_order_off + (size_t)8 * p.order_slots * sizeof(int32_t);
@@ -411,6 +427,16 @@ csr_status csr_set_attention_events(void* begin_event, void* end_event) {
     return fail(CSR_E_INVAL, "set both events or neither");
   g_ev_begin = static_cast<hipEvent_t>(begin_event);
   g_ev_end = static_cast<hipEvent_t>(end_event);
+  return CSR_OK;
+}
+
+csr_status csr_set_plan_overrides(int32_t nsplit, int32_t fixed_order, int32_t dma_all_waves) {
+  if (nsplit < 0 || (fixed_order != 0 && fixed_order != 1) || (dma_all_waves != 0 && dma_all_waves != 1))
+    return fail(CSR_E_INVAL, "plan overrides: nsplit >= 0, flags 0 or 1 (got %d, %d, %d)", nsplit, fixed_order,
+                dma_all_waves);
+  g_ovr.nsplit = nsplit;
+  g_ovr.fixed_order = fixed_order;
+  g_ovr.dma_all_waves = dma_all_waves;
   return CSR_OK;
 }
 

@@ -690,7 +690,9 @@ __global__ void __launch_bounds__(NW * 64, 8 / NW) attn_bf16_kernel(const AttnAr
       const auto pr = __builtin_amdgcn_permlane32_swap(__float_as_uint(mx), __float_as_uint(mx), false, false);
       const float mxs = __builtin_elementwise_maximum(__uint_as_float(pr[0]), __uint_as_float(pr[1])) * c;
       const float mnew = fmaxf(mref, mxs);
-      const float alpha = fast_exp2((mref == -INFINITY ? 0.f : mref) - (mnew == -INFINITY ? 0.f : mnew));
+      // With no reference yet (mref = -inf) nothing has been accumulated: the
+      // factor is 0, not exp2(-mnew), which overflows for very low scores.
+      const float alpha = mref == -INFINITY ? 0.f : fast_exp2(mref - mnew);
       lrow *= alpha;
 #pragma unroll
       for (int db = 0; db < DB; ++db) o[db] *= alpha;

@@ -101,7 +101,7 @@ struct RopeArgs {
   int32_t kv8;               // keys/values (outputs and cache) are e4m3 codes; bf16 inputs
   int32_t q8;                // kv8 only: q rows are quantised too (q_out holds e4m3 codes)
   float inv_k, inv_v, inv_q;  // fp32(1 / k_scale), fp32(1 / v_scale), fp32(1 / q_scale)
-  double half_turns[64];     // theta_i / pi for i < rdim / 2
+  double inv_freq[64];       // theta_i = pow(theta, -2i / rdim) in fp64, i < rdim / 2 (pair i turns by pos * theta_i)
 };
 hipError_t launch_rope_append(const RopeArgs& a, int dtype_bf16, hipStream_t stream);
 

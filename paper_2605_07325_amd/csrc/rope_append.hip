@@ -18,16 +18,19 @@
 // (decode) spread one token over several workgroups, one piece per thread;
 // long ones use one workgroup per token that loops over its pieces, so the
 // angles are formed once per token.  The token's sequence and position are
-// uniform over the workgroup.  The first r/2 threads form (cos, sin) of each pair angle
-// pos * theta_i into LDS: the angle is reduced to half-turns in [-1, 1] in
-// fp64 (pos * theta_i / pi, minus the nearest even integer), then sincospif
-// evaluates it in fp32, so the phase error stays ~1e-7 rad even at positions
-// near 2^17 where a plain fp32 product would be off by ~1e-2 rad.  Every
-// thread then takes 8-element pieces of the token's rows: a neox piece rotates
-// elements [e, e+8) against [e + r/2, e + r/2 + 8), an interleaved piece
-// rotates the four pairs inside [e, e+8), tail pieces (dims >= r) and value
-// rows are copied bit for bit.  Loads and stores are 16 bytes per lane, and
-// consecutive lanes take consecutive pieces of a row.
+// uniform over the workgroup.  The first r/2 threads form (cos, sin) of each
+// pair angle pos * theta_i into LDS in fp64 (theta_i comes from the host as
+// the double pow(theta, -2i/r)).  Every thread then takes 8-element pieces of
+// the token's rows: a neox piece rotates elements [e, e+8) against
+// [e + r/2, e + r/2 + 8), an interleaved piece rotates the four pairs inside
+// [e, e+8), tail pieces (dims >= r) and value rows are copied bit for bit.
+// The rotation itself is fp64 (x cos - x' sin, each product rounded, no fused
+// multiply-add) and each result is rounded once to the element type: bf16
+// directly from fp64, nearest even; fp32 by the plain conversion; an fp8 code
+// from the fp32 value.  The rotated values therefore depend on the inputs and
+// on how closely cos and sin are evaluated, not on any fp32 intermediate.
+// Loads and stores are 16 bytes per lane, and consecutive lanes take
+// consecutive pieces of a row.
 #include "kernels.h"
 
 namespace csr {
@@ -38,6 +41,7 @@ typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
 typedef float f32x2 __attribute__((ext_vector_type(2)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef double f64x2 __attribute__((ext_vector_type(2)));
 typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 
 __device__ __forceinline__ int token_sequence(const int32_t* __restrict__ cu, int batch, int tok) {
@@ -79,6 +83,39 @@ __device__ __forceinline__ void load8(const void* base, int64_t e, float (&x)[8]
   }
 }
 
+// bf16 bit pattern of the nearest bf16 value to v (ties to even), rounded
+// once, directly from fp64.  Normal range: round the fp64 bit pattern at the
+// 8th significant bit (bit 45 of the fraction); below 2^-126, where bf16 steps
+// are 2^-133, scale by 2^133 (exact), round to an integer and scale back.
+__device__ __forceinline__ uint32_t bf16_bits_of(double v) {
+  if (v != v) return 0x7fc0u;
+  const double a = fabs(v);
+  const uint32_t sign = v < 0.0 ? 0x8000u : 0u;
+  if (a < 0x1p-126) {
+    const double q = rint(a * 0x1p133) * 0x1p-133;  // exact in fp32
+    return sign | (__float_as_uint((float)q) >> 16);
+  }
+  uint64_t b = (uint64_t)__double_as_longlong(a);
+  b += 0xFFFFFFFFFFFull + ((b >> 45) & 1ull);  // ties to even at bit 45
+  b &= ~0x1FFFFFFFFFFFull;
+  const double r = __longlong_as_double((long long)b);
+  if (r > 0x1.FEp127) return sign | 0x7f80u;  // beyond the largest bf16: infinity
+  return sign | (__float_as_uint((float)r) >> 16);  // exact: r is a bf16 value
+}
+
+template <bool BF16>
+__device__ __forceinline__ void store8d(void* base, int64_t e, const double (&y)[8]) {
+  if constexpr (BF16) {
+    const u32x4 w = {bf16_bits_of(y[0]) | (bf16_bits_of(y[1]) << 16), bf16_bits_of(y[2]) | (bf16_bits_of(y[3]) << 16),
+                     bf16_bits_of(y[4]) | (bf16_bits_of(y[5]) << 16), bf16_bits_of(y[6]) | (bf16_bits_of(y[7]) << 16)};
+    *reinterpret_cast<u32x4*>(static_cast<uint16_t*>(base) + e) = w;
+  } else {
+    f32x4* p = reinterpret_cast<f32x4*>(static_cast<float*>(base) + e);
+    p[0] = f32x4{(float)y[0], (float)y[1], (float)y[2], (float)y[3]};
+    p[1] = f32x4{(float)y[4], (float)y[5], (float)y[6], (float)y[7]};
+  }
+}
+
 template <bool BF16>
 __device__ __forceinline__ void store8(void* base, int64_t e, const float (&y)[8]) {
   if constexpr (BF16) {
@@ -113,6 +150,14 @@ __device__ __forceinline__ void store8q(void* base, int64_t e, const float (&y)[
   *reinterpret_cast<u32x2*>(static_cast<uint8_t*>(base) + e) = u32x2{w[0], w[1]};
 }
 
+// 8 fp64 values, each rounded to fp32, scaled by inv and quantised.
+__device__ __forceinline__ void store8qd(void* base, int64_t e, const double (&y)[8], float inv) {
+  float f[8];
+#pragma unroll
+  for (int j = 0; j < 8; ++j) f[j] = (float)y[j];
+  store8q(base, e, f, inv);
+}
+
 // Bit copy of 8 elements (tail dims, value rows).
 template <bool BF16>
 __device__ __forceinline__ void copy8(void* dst, const void* src, int64_t de, int64_t se) {
@@ -124,8 +169,9 @@ __device__ __forceinline__ void copy8(void* dst, const void* src, int64_t de, in
 }
 
 template <bool BF16, bool KV8>
-__device__ __forceinline__ void rotate_piece(const RopeArgs& a, const f32x2* cs, int tok, int64_t slot, int u,
+__device__ __forceinline__ void rotate_piece(const RopeArgs& a, const f64x2* cs, int tok, int64_t slot, int u,
                                              int rot_units, int per_row, int n_rot, int nq, bool neox) {
+#pragma clang fp contract(off)
   const int d = a.d;
   const int half = a.rdim >> 1;
   if (u >= rot_units) {  // value row piece: into the cache (and, quantised, the workspace)
@@ -157,6 +203,10 @@ __device__ __forceinline__ void rotate_piece(const RopeArgs& a, const f32x2* cs,
     if (quant) store8q(base, e, y, inv);
     else store8<BF16>(base, e, y);
   };
+  auto putd = [&](void* base, int64_t e, const double (&y)[8]) {
+    if (quant) store8qd(base, e, y, inv);
+    else store8d<BF16>(base, e, y);
+  };
   if (piece >= n_rot) {  // dims >= r: unchanged (quantised for an fp8 cache)
     const int e = a.rdim + ((piece - n_rot) << 3);
     if (quant) {
@@ -170,53 +220,58 @@ __device__ __forceinline__ void rotate_piece(const RopeArgs& a, const f32x2* cs,
     }
     return;
   }
+  // x cos - x' sin and x' cos + x sin in fp64, each product rounded separately
+  // (no contraction into fused multiply-adds: see the pragma at the top).
   if (neox) {
     const int e0 = piece << 3, e1 = e0 + half;
-    float x0[8], x1[8], y0[8], y1[8];
+    float x0[8], x1[8];
+    double y0[8], y1[8];
     load8<BF16>(src, row + e0, x0);
     load8<BF16>(src, row + e1, x1);
 #pragma unroll
     for (int j = 0; j < 8; ++j) {
-      const f32x2 t = cs[e0 + j];
-      y0[j] = fmaf(x0[j], t[0], -x1[j] * t[1]);
-      y1[j] = fmaf(x1[j], t[0], x0[j] * t[1]);
+      const f64x2 t = cs[e0 + j];
+      const double u0 = x0[j], u1 = x1[j];
+      y0[j] = u0 * t[0] - u1 * t[1];
+      y1[j] = u1 * t[0] + u0 * t[1];
     }
     if (out) {
-      put(out, row + e0, y0);
-      put(out, row + e1, y1);
+      putd(out, row + e0, y0);
+      putd(out, row + e1, y1);
     }
     if (pool) {
-      put(pool, prow + e0, y0);
-      put(pool, prow + e1, y1);
+      putd(pool, prow + e0, y0);
+      putd(pool, prow + e1, y1);
     }
   } else {
     const int e0 = piece << 3;
-    float x[8], y[8];
+    float x[8];
+    double y[8];
     load8<BF16>(src, row + e0, x);
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
-      const f32x2 t = cs[(e0 >> 1) + j];
-      y[2 * j] = fmaf(x[2 * j], t[0], -x[2 * j + 1] * t[1]);
-      y[2 * j + 1] = fmaf(x[2 * j + 1], t[0], x[2 * j] * t[1]);
+      const f64x2 t = cs[(e0 >> 1) + j];
+      const double u0 = x[2 * j], u1 = x[2 * j + 1];
+      y[2 * j] = u0 * t[0] - u1 * t[1];
+      y[2 * j + 1] = u1 * t[0] + u0 * t[1];
     }
-    if (out) put(out, row + e0, y);
-    if (pool) put(pool, prow + e0, y);
+    if (out) putd(out, row + e0, y);
+    if (pool) putd(pool, prow + e0, y);
   }
 }
 
 template <bool BF16, bool KV8>
 __global__ void __launch_bounds__(256) rope_append_kernel(RopeArgs a) {
-  __shared__ f32x2 cs[64];
+  __shared__ f64x2 cs[64];
   const int tok = blockIdx.x;
   const int b = token_sequence(a.cu_q, a.batch, tok);
   const int64_t pos = (int64_t)(a.cache_len ? a.cache_len[b] : 0) + (tok - a.cu_q[b]);
   const int half = a.rdim >> 1;
   if ((int)threadIdx.x < half) {
-    double t = (double)pos * a.half_turns[threadIdx.x];  // angle / pi
-    t -= 2.0 * rint(0.5 * t);                             // same angle, now in [-1, 1]
-    float s, c;
-    sincospif((float)t, &s, &c);
-    cs[threadIdx.x] = f32x2{c, s};
+    const double angle = (double)pos * a.inv_freq[threadIdx.x];
+    double s, c;
+    sincos(angle, &s, &c);
+    cs[threadIdx.x] = f64x2{c, s};
   }
 
   // Cache slot of this token (pool writes only); an invalid page drops them.

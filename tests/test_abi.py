@@ -214,3 +214,48 @@ def test_fp8_cache_workspace_holds_quantised_chunk():
                            q_scale=0.015625, **over)
             assert (csr.extend_workspace_size(q8, 1, T, T, L) - base
                     == extra + align(T * 64 * 128) + 2 * align(T * 4 * 128))
+
+
+def test_plan_overrides_validation():
+    lib = csr.lib()
+    assert lib.csr_set_plan_overrides(-1, 0, 0) == csr.CSR_E_INVAL
+    assert lib.csr_set_plan_overrides(0, 2, 0) == csr.CSR_E_INVAL
+    assert lib.csr_set_plan_overrides(0, 0, -1) == csr.CSR_E_INVAL
+    assert lib.csr_set_plan_overrides(0, 0, 0) == csr.CSR_OK
+
+
+def test_plan_overrides_steer_the_split_and_the_environment_does_not():
+    """Forcing 4 key splits sizes the split-K partials for 4; the planner's own choice
+    comes back afterwards, and an environment variable of the old override names
+    changes nothing."""
+    d = good_desc(num_q_heads=64, num_kv_heads=4)
+    args = (1, 512, 512, 122880)
+    base = csr.extend_workspace_size(d, *args)
+    with csr.plan_overrides(nsplit=4):
+        forced = csr.extend_workspace_size(d, *args)
+    rows = 512 * 64
+    want = ((4 * rows * 128 * 4 + 255) // 256) * 256 + 4 * rows * 4
+    assert forced == want
+    assert csr.extend_workspace_size(d, *args) == base
+    os.environ["CSR_NSPLIT"] = "7"
+    try:
+        assert csr.extend_workspace_size(d, *args) == base
+    finally:
+        os.environ.pop("CSR_NSPLIT", None)
+
+
+def test_binding_rejects_pools_of_another_layout():
+    """num_pages bounds every page id the kernels read, so the binding accepts only
+    [num_pages][P][Hkv][d] pools of the descriptor's element type."""
+    d = good_desc()
+    flat = torch.zeros((64 * 16, 2, 128), dtype=torch.bfloat16)
+    with pytest.raises(ValueError):
+        csr._pool_pages(d, flat, flat)
+    wrong_type = torch.zeros((64, 16, 2, 128), dtype=torch.float32)
+    with pytest.raises(ValueError):
+        csr._pool_pages(d, wrong_type, wrong_type)
+    ok = torch.zeros((64, 16, 2, 128), dtype=torch.bfloat16)
+    with pytest.raises(ValueError):  # right layout, but a host tensor
+        csr._pool_pages(d, ok, ok)
+    with pytest.raises(ValueError):
+        csr._pool_pages(d, None, ok)

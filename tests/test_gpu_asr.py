@@ -127,3 +127,5 @@ def test_one_reconciliation_cycle(partitioned):
     assert torch.equal(rk.view(torch.int16), fk.view(torch.int16))
     assert torch.equal(rv.view(torch.int16), fv.view(torch.int16))
     note(f"asr reconciled cache ({len(seq)} positions) equals a one-shot prefill bit for bit")
+    del rec
+    asr.destroy_streams(ps, ss)

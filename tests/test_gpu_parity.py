@@ -5,27 +5,16 @@ checked on every output row (several row tiles, ragged tails, split-K forced);
 the full-size workloads on seeded sampled rows.  Appends are compared bit for
 bit over the whole pool.
 """
-import os
-
 import numpy as np
 import pytest
 import torch
 
 from oracle import oracle
+from paper_2605_07325_amd import csr
 from paper_2605_07325_amd import datagen as dg
 from tests.gpu_harness import Dev, compare, from_dev, note, oracle_rows
 
 pytestmark = pytest.mark.gpu
-
-
-@pytest.fixture(autouse=True)
-def _no_split_override():
-    saved = {k: os.environ.pop(k, None) for k in ("CSR_NSPLIT",)}
-    yield
-    for k, v in saved.items():
-        os.environ.pop(k, None)
-        if v is not None:
-            os.environ[k] = v
 
 
 SMALL = [
@@ -68,7 +57,7 @@ SMALL = [
 @pytest.mark.parametrize("nsplit", [None, 3])
 def test_small_shapes_all_rows(label, kw, nsplit):
     if nsplit:
-        os.environ["CSR_NSPLIT"] = str(nsplit)
+        csr.set_plan_overrides(nsplit=nsplit)
     case = dg.make_case(label, seed=1, cfg_id=300, **kw)
     note(f"{label} nsplit={nsplit} L={case.cache_len.tolist()} n={case.seqlen_q.tolist()}: csr_extend_attention")
     dev = Dev(case)
@@ -170,7 +159,7 @@ DECODE = [
 @pytest.mark.parametrize("nsplit", [None, 5, 16])
 def test_short_chunks_all_rows(label, kw, nsplit):
     if nsplit:
-        os.environ["CSR_NSPLIT"] = str(nsplit)
+        csr.set_plan_overrides(nsplit=nsplit)
     case = dg.make_case(label, seed=2, cfg_id=310, **kw)
     note(f"{label} nsplit={nsplit} L={case.cache_len.tolist()} n={case.seqlen_q.tolist()}")
     dev = Dev(case)
@@ -192,13 +181,10 @@ def test_short_chunks_dma_issuers_do_not_change_results(label, kw):
     case = dg.make_case(label, seed=2, cfg_id=311, **kw)
     note(f"{label}: K/V loads from the upper waves vs from every wave")
     outs = []
-    for flag in ("1", "0"):
-        os.environ["CSR_DMA_UPPER"] = flag
-        try:
+    for all_waves in (False, True):
+        with csr.plan_overrides(dma_all_waves=all_waves):
             out, lse = Dev(case).extend()
             torch.cuda.synchronize()
-        finally:
-            os.environ.pop("CSR_DMA_UPPER", None)
         outs.append((out.view(torch.int16).cpu(), lse.cpu()))
     assert torch.equal(outs[0][0], outs[1][0]) and torch.equal(outs[0][1], outs[1][1])
 

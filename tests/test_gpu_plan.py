@@ -6,8 +6,6 @@ row tile holds rows runs exactly once), slot w on XCD w % 8, and each XCD's
 queue longest first (within the length spread of one subgroup of row tiles).
 """
 import math
-import os
-
 import numpy as np
 import pytest
 import torch
@@ -19,15 +17,6 @@ from tests.gpu_harness import Dev, compare, note, oracle_rows
 pytestmark = pytest.mark.gpu
 
 BM = 256  # packed rows per workgroup of the bf16 kernel (chunks longer than 8 tokens at G = 16)
-
-
-@pytest.fixture(autouse=True)
-def _restore_env():
-    saved = os.environ.pop("CSR_NSPLIT", None)
-    yield
-    os.environ.pop("CSR_NSPLIT", None)
-    if saved is not None:
-        os.environ["CSR_NSPLIT"] = saved
 
 
 def subgroup_rows(batch, hkv, mtiles):
@@ -80,7 +69,7 @@ def check_order(case, dev, nsplit, L, n):
 
 @pytest.mark.parametrize("nsplit", [1, 3])
 def test_work_order_is_a_longest_first_permutation(nsplit):
-    os.environ["CSR_NSPLIT"] = str(nsplit)
+    csr.set_plan_overrides(nsplit=nsplit)
     g = np.random.default_rng(17)
     L = g.integers(0, 20000, size=7)
     n = g.integers(9, 700, size=7)
@@ -95,7 +84,7 @@ def test_work_order_at_the_group_limit_with_wider_subgroups():
     """256 sequences x 4 kv heads = 1024 groups (the most one plan takes) of up to 7 row
     tiles: 10 row tiles per subgroup; the order is checked as above and the outputs of
     five sequences on every row against the oracle."""
-    os.environ["CSR_NSPLIT"] = "1"
+    csr.set_plan_overrides(nsplit=1)
     g = np.random.default_rng(23)
     B = 256
     L = g.integers(0, 400, size=B)
