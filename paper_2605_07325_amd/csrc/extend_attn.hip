@@ -168,10 +168,13 @@ struct Unit {
 
 template <int BM>
 __device__ __forceinline__ bool decode_unit(const AttnArgs& a, Unit& u) {
+  // The unit's description is read through the constant address space
+  // (scalar loads): every field is then wave-uniform by construction.
+  typedef const __attribute__((address_space(4))) int32_t* cptr;
   const int w = blockIdx.x;
   int r = w;
   if (a.order) {
-    r = a.order[w];  // planned on the device (ragged batches): -1 = no unit
+    r = ((cptr)a.order)[w];  // planned on the device (ragged batches): -1 = no unit
     if (r < 0) return false;
   } else if (a.xcd_remap) {
     const int q8 = gridDim.x >> 3;  // grid is padded to a multiple of 8
@@ -185,9 +188,9 @@ __device__ __forceinline__ bool decode_unit(const AttnArgs& a, Unit& u) {
   u.g = rest % a.Hkv;
   u.b = rest / a.Hkv;
   mt = a.mtiles - 1 - mt;  // later rows see more keys: issue them first
-  u.cuq = a.cu_q[u.b];
-  u.n = a.cu_q[u.b + 1] - u.cuq;
-  u.L = a.cache_len ? a.cache_len[u.b] : 0;
+  u.cuq = ((cptr)a.cu_q)[u.b];
+  u.n = ((cptr)a.cu_q)[u.b + 1] - u.cuq;
+  u.L = a.cache_len ? ((cptr)a.cache_len)[u.b] : 0;
   u.rows_total = u.n * a.G;
   u.m0 = mt * BM;
   if (u.m0 >= u.rows_total) return false;
@@ -359,7 +362,8 @@ __global__ void __launch_bounds__(NW * 64, 8 / NW) attn_bf16_kernel(const AttnAr
   // A wave whose 32 rows are all padding (short chunks: n*G < BM) skips the
   // products and exponentials but still issues its share of every K/V DMA
   // and joins every barrier.
-  const bool wave_active = (!DMA_UPPER || wave < NW / 2) && u.m0 + wave * 32 < u.rows_total;
+  const bool wave_active =
+      __builtin_amdgcn_readfirstlane((!DMA_UPPER || wave < NW / 2) && u.m0 + wave * 32 < u.rows_total ? 1 : 0) != 0;
   const int tok = m_row / G;
   const int lim = u.L + tok;  // last key this lane's row sees
   {
@@ -427,6 +431,17 @@ __global__ void __launch_bounds__(NW * 64, 8 / NW) attn_bf16_kernel(const AttnAr
     const int pidx = t >> log2P;
     return bt ? bt[pidx] : bt_base + pidx;
   };
+  // The same for a key known to lie inside the table row (t < L + n): no
+  // test, and the contiguous cache (no table) by a select, not a branch (the
+  // row's first entry is read instead, and discarded).
+  const_i32p bt_row = bt ? bt : (const_i32p)a.cu_q;
+  const int bt_any = bt ? -1 : 0;
+
+  auto page_id_in_row = [&](int tile, int g) -> int {
+    const int pidx = block_key(tile, g) >> log2P;
+    const int v = bt_row[pidx & bt_any];
+    return bt_any ? v : bt_base + pidx;
+  };
   auto page_off = [&](int tile, int g, int pg) -> int64_t {
     const int t = block_key(tile, g);
     pg = (uint32_t)pg < (uint32_t)num_pages ? pg : 0;
@@ -440,10 +455,15 @@ __global__ void __launch_bounds__(NW * 64, 8 / NW) attn_bf16_kernel(const AttnAr
   // inside the prefix or wholly inside the chunk takes a scalar base plus the
   // lanes' constant 32-bit offsets; a tile straddling L or ending the key
   // range selects per lane.
-  auto issue_group = [&](int tile, int g, int64_t pgoff, char* dst, const char* pool_base, const char* new_base) {
+  auto issue_group = [&](int tile, int g, int64_t pgoff, char* dst, const char* pool_base, const char* new_base,
+                         auto pfx) {
     const int t0 = tile * KT;
     if constexpr (SCALAR_PAGES) {
       const uint32_t m0 = lds_addr(dst) + blk(g * PB) * 1024;
+      if constexpr (decltype(pfx)::value) {  // caller guarantees a wholly cached tile
+        dma_sbase<PB>(pool_base + pgoff, m0, &pool_v[g * PB]);
+        return;
+      }
       if (t0 + KT - 1 < u.L) {
         dma_sbase<PB>(pool_base + pgoff, m0, &pool_v[g * PB]);
         return;
@@ -470,7 +490,7 @@ __global__ void __launch_bounds__(NW * 64, 8 / NW) attn_bf16_kernel(const AttnAr
   auto issue = [&](int tile, const int64_t* pg, char* dst, const char* pool_base, const char* new_base) {
     if (!dma_wave) return;
 #pragma unroll
-    for (int g = 0; g < NPG; ++g) issue_group(tile, g, pg[g], dst, pool_base, new_base);
+    for (int g = 0; g < NPG; ++g) issue_group(tile, g, pg[g], dst, pool_base, new_base, std::false_type{});
   };
   // K ring first: its stage and block offsets then fit the 16-bit DS offset
   // field; the V ring's base is folded into the per-lane V read addresses.
@@ -655,21 +675,20 @@ __global__ void __launch_bounds__(NW * 64, 8 / NW) attn_bf16_kernel(const AttnAr
             __builtin_bit_cast(bf16x8, u32x4{w[hf][db][0][0], w[hf][db][0][1], w[hf][db][1][0], w[hf][db][1][1]}),
             __builtin_bit_cast(bf16x8, pf[hf]), o[db], 0, 0, 0);
   };
-  // exp2(s*c - m) packed to bf16 for contraction half hf (8 keys); adds the row sums.
-  auto exp_half = [&](const f32x16& s, int hf) -> u32x4 {
+  // exp2(s*c - m) packed to bf16 for contraction half hf (8 keys), and their
+  // sum (a tree: no dependent chain through all eight).
+  auto exp_half = [&](const f32x16& s, int hf, float& bs) -> u32x4 {
     float p[8];
 #pragma unroll
     for (int e = 0; e < 8; ++e) p[e] = fast_exp2(__builtin_fmaf(s[8 * hf + e], c, neg_m));
-    const u32x4 r{pack_bf16x2(p[0], p[1]), pack_bf16x2(p[2], p[3]), pack_bf16x2(p[4], p[5]), pack_bf16x2(p[6], p[7])};
-    float rs = 0.f;
-#pragma unroll
-    for (int e = 0; e < 8; ++e) rs += p[e];
-    lrow += rs;
-    return r;
+    bs = ((p[0] + p[1]) + (p[2] + p[3])) + ((p[4] + p[5]) + (p[6] + p[7]));
+    return u32x4{pack_bf16x2(p[0], p[1]), pack_bf16x2(p[2], p[3]), pack_bf16x2(p[4], p[5]), pack_bf16x2(p[6], p[7])};
   };
   auto softmax_exp = [&](const f32x16& s, u32x4* pf) {
-    pf[0] = exp_half(s, 0);
-    pf[1] = exp_half(s, 1);
+    float b0, b1;
+    pf[0] = exp_half(s, 0, b0);
+    pf[1] = exp_half(s, 1, b1);
+    lrow += b0 + b1;
   };
   // Pins a value at this point of the program: IR-level sinking would
   // otherwise move the exponentials past the DMA branches to their use by the
@@ -677,11 +696,12 @@ __global__ void __launch_bounds__(NW * 64, 8 / NW) attn_bf16_kernel(const AttnAr
   auto pin = [](u32x4& x) { asm volatile("" : "+v"(x)); };
   // Maximum of the lane's 16 raw scores (half of its row's 32 keys).
   auto row_max = [&](const f32x16& s) -> float {
-    float mx = __builtin_elementwise_maximum(s[0], s[1]);
-#pragma unroll
-    for (int v = 2; v < 16; v += 2)
-      mx = __builtin_elementwise_maximum(mx, __builtin_elementwise_maximum(s[v], s[v + 1]));
-    return mx;
+    auto mx3 = [](float a, float b, float c) {
+      return __builtin_elementwise_maximum(__builtin_elementwise_maximum(a, b), c);
+    };
+    const float u0 = mx3(mx3(s[0], s[1], s[2]), mx3(s[3], s[4], s[5]), mx3(s[6], s[7], s[8]));
+    const float u1 = mx3(mx3(s[9], s[10], s[11]), mx3(s[12], s[13], s[14]), s[15]);
+    return __builtin_elementwise_maximum(u0, u1);
   };
   // Move the reference max if any lane's scores grew past the threshold; only
   // then is the exact row max (both half-rows) formed.
@@ -701,6 +721,28 @@ __global__ void __launch_bounds__(NW * 64, 8 / NW) attn_bf16_kernel(const AttnAr
       thr = (mnew + THRESH) / c;
     }
   };
+  // Main-loop check of a block's probabilities instead of its row max: if in
+  // some lane the 16 of them (formed against the current reference) sum past
+  // 2^16, or to NaN, form the block's exact row max, move the reference,
+  // rescale the row sum and recompute the probabilities; alpha then rescales
+  // O (by the caller, outside this branch, so that O keeps its registers).
+  // Every probability used stays below 2^16, and as with the lazily moved
+  // maximum the final normalisation is exact whatever reference was used.
+  auto reexp = [&](const f32x16& s, u32x4* pf, float& bsum, float& alpha) {
+    const float mx = row_max(s);
+    const auto pr = __builtin_amdgcn_permlane32_swap(__float_as_uint(mx), __float_as_uint(mx), false, false);
+    const float mxs = __builtin_elementwise_maximum(__uint_as_float(pr[0]), __uint_as_float(pr[1])) * c;
+    const float mnew = fmaxf(mref, mxs);
+    alpha = mref == -INFINITY ? 0.f : fast_exp2(mref - mnew);
+    lrow *= alpha;
+    mref = mnew;
+    neg_m = mnew == -INFINITY ? 0.f : -mnew;
+    thr = (mnew + THRESH) / c;
+    float b0, b1;
+    pf[0] = exp_half(s, 0, b0);
+    pf[1] = exp_half(s, 1, b1);
+    bsum = b0 + b1;
+  };
   // One pipelined block step: exponentials of s_cur (block kb of V tile vl)
   // against the scores of the next block (block kb_next of K tile kl_next).
   // Each step also issues two DMA blocks (dma_a, dma_b), one after each half
@@ -713,25 +755,34 @@ __global__ void __launch_bounds__(NW * 64, 8 / NW) attn_bf16_kernel(const AttnAr
                   const char* kl_after, int kb_after, auto dma_a, auto dma_b) {
     u32x4 pf[2];
     KF kh1[DS / 2];
+    float b0, b1;
     s_next = f32x16{};
     load_k(kl_next, kb_next, DS / 2, kh1);
     __builtin_amdgcn_sched_barrier(0);
-    pf[0] = exp_half(s_cur, 0);
+    pf[0] = exp_half(s_cur, 0, b0);
     mfma_k(kpre, 0, s_next);
     pin(pf[0]);
     __builtin_amdgcn_sched_barrier(0);
     dma_a();
     __builtin_amdgcn_sched_barrier(0);
-    pf[1] = exp_half(s_cur, 1);
+    pf[1] = exp_half(s_cur, 1, b1);
     mfma_k(kh1, DS / 2, s_next);
     pin(pf[1]);
+    __builtin_amdgcn_sched_barrier(0);
+    float bsum = b0 + b1, alpha = 1.f;
+    const bool redo = __any(!(bsum <= 65536.f));
+    if (redo) reexp(s_cur, pf, bsum, alpha);
+    lrow += bsum;
     __builtin_amdgcn_sched_barrier(0);
     dma_b();
     __builtin_amdgcn_sched_barrier(0);
     load_k(kl_after, kb_after, 0, kpre);
     __builtin_amdgcn_sched_barrier(0);
+    if (redo) {
+#pragma unroll
+      for (int db = 0; db < DB; ++db) o[db] *= alpha;
+    }
     pv_asm(voff_c, pf);
-    update_ref(row_max(s_next));
     s_cur = s_next;
   };
 
@@ -769,9 +820,17 @@ __global__ void __launch_bounds__(NW * 64, 8 / NW) attn_bf16_kernel(const AttnAr
       update_ref(row_max(s_a));
       load_k(kring, 1, 0, kpre);
     }
-    // Tile k with ring stage S = k % 4 known at compile time.
-    auto tile = [&](int k, auto stage) {
+    // Tile k with ring stage S = k % 4 known at compile time; ACT: the wave
+    // holds rows (else it only issues its share of the DMA and joins the
+    // barriers).  Active and row-less waves run separate copies of the loop, so
+    // the compiler's wait counting in the active loop never merges with the
+    // row-less path's scalar loads.
+    // PFX: the tile whose DMA this tile issues (tb+k+3) lies wholly in the
+    // cached prefix, so is the one whose page id it loads (tb+k+4) inside the
+    // table row: neither needs a test.
+    auto tile = [&](int k, auto stage, auto act, auto pfx) {
       constexpr int S = decltype(stage)::value;
+      constexpr bool ACT = decltype(act)::value;
       // Tiles k and k+1 have landed in LDS (only the previous tile's DMA may
       // still be in flight) and this wave's LDS reads of tile k-1 are done.
       // A plain s_barrier: __syncthreads() would also fence, i.e. wait for the
@@ -779,6 +838,15 @@ __global__ void __launch_bounds__(NW * 64, 8 / NW) attn_bf16_kernel(const AttnAr
       if constexpr (SCALAR_PAGES) asm volatile("s_waitcnt vmcnt(%0) lgkmcnt(0)" ::"n"(2 * NDMA) : "memory");
       else asm volatile("s_waitcnt vmcnt(0) lgkmcnt(0)" ::: "memory");
       __builtin_amdgcn_s_barrier();
+      // The page ids loaded during the previous tile have arrived (the wait
+      // above); passing them through an empty asm tells the compiler so, which
+      // keeps it from waiting for them, and with them for every LDS read
+      // issued meanwhile, at their first use.
+#pragma unroll
+      for (int g = 0; g < NPG; ++g) {
+        if constexpr (SCALAR_PAGES) asm volatile("" : "+s"(pgi[g]));
+        else asm volatile("" : "+v"(pgi[g]));
+      }
       // K/V(tb+k+3) replace K/V(tb+k-1), last read during tile k-1; their
       // DMA blocks are spread over the tile's two steps.
       const int nt = clampt(u.tb + k + 3);
@@ -792,30 +860,33 @@ __global__ void __launch_bounds__(NW * 64, 8 / NW) attn_bf16_kernel(const AttnAr
       auto kd0 = [&] {
         if (!dma_wave) return;
 #pragma unroll
-        for (int g = 0; g < NG0; ++g) issue_group(nt, g, pgn[g], kdst, kpool, knew);
+        for (int g = 0; g < NG0; ++g) issue_group(nt, g, pgn[g], kdst, kpool, knew, pfx);
       };
       auto kd1 = [&] {
         if (!dma_wave) return;
 #pragma unroll
-        for (int g = NG0; g < NPG; ++g) issue_group(nt, g, pgn[g], kdst, kpool, knew);
+        for (int g = NG0; g < NPG; ++g) issue_group(nt, g, pgn[g], kdst, kpool, knew, pfx);
       };
       auto vd0 = [&] {
         if (!dma_wave) return;
 #pragma unroll
-        for (int g = 0; g < NG0; ++g) issue_group(nt, g, pgn[g], vdst, vpool, vnew);
+        for (int g = 0; g < NG0; ++g) issue_group(nt, g, pgn[g], vdst, vpool, vnew, pfx);
       };
       auto vd1 = [&] {
         if (!dma_wave) return;
 #pragma unroll
-        for (int g = NG0; g < NPG; ++g) issue_group(nt, g, pgn[g], vdst, vpool, vnew);
+        for (int g = NG0; g < NPG; ++g) issue_group(nt, g, pgn[g], vdst, vpool, vnew, pfx);
 #pragma unroll
-        for (int g = 0; g < NPG; ++g) pgi[g] = page_id(clampt(u.tb + k + 4), g);
+        for (int g = 0; g < NPG; ++g) {
+          if constexpr (SCALAR_PAGES && decltype(pfx)::value) pgi[g] = page_id_in_row(clampt(u.tb + k + 4), g);
+          else pgi[g] = page_id(clampt(u.tb + k + 4), g);
+        }
       };
       // The two waves of a SIMD take turns at the higher issue priority, one
       // step each, so that neither lags the other into the tile barrier.
       if (wave < NW / 2) __builtin_amdgcn_s_setprio(1); else __builtin_amdgcn_s_setprio(0);
       // block 0 || scores of block 1, then block 1 || scores of the next tile's block 0
-      if (!wave_active) {
+      if constexpr (!ACT) {
         kd0(); kd1(); vd0(); vd1();
         return;
       }
@@ -824,15 +895,33 @@ __global__ void __launch_bounds__(NW * 64, 8 / NW) attn_bf16_kernel(const AttnAr
       step(s_a, s_b, std::integral_constant<int, S * TILEB + 32 * ROWB>{}, kring + ((S + 1) % ST) * TILEB, 0,
            kring + ((S + 1) % ST) * TILEB, 1, vd0, vd1);
     };
-    for (int k = 0; k < n_main; k += 4) {
-      tile(k, std::integral_constant<int, 0>{});
-      if (k + 1 >= n_main) break;
-      tile(k + 1, std::integral_constant<int, 1>{});
-      if (k + 2 >= n_main) break;
-      tile(k + 2, std::integral_constant<int, 2>{});
-      if (k + 3 >= n_main) break;
-      tile(k + 3, std::integral_constant<int, 3>{});
-    }
+    // Iterations whose DMA target tile (tb+k+3, clamped) lies wholly in the
+    // cached prefix run first, in whole rounds of the ring, without the
+    // per-tile classification; the rest take the general path.
+    const int pfx_tiles = u.L / KT;  // tiles [0, pfx_tiles) are wholly cached
+    const int k_pfx = main_end - 1 < pfx_tiles ? n_main : max(0, min(n_main, pfx_tiles - u.tb - 3));
+    auto tiles = [&](auto act) {
+      int k = 0;
+      if constexpr (SCALAR_PAGES) {
+        for (; k + 4 <= k_pfx; k += 4) {
+          tile(k, std::integral_constant<int, 0>{}, act, std::true_type{});
+          tile(k + 1, std::integral_constant<int, 1>{}, act, std::true_type{});
+          tile(k + 2, std::integral_constant<int, 2>{}, act, std::true_type{});
+          tile(k + 3, std::integral_constant<int, 3>{}, act, std::true_type{});
+        }
+      }
+      for (; k < n_main; k += 4) {
+        tile(k, std::integral_constant<int, 0>{}, act, std::false_type{});
+        if (k + 1 >= n_main) break;
+        tile(k + 1, std::integral_constant<int, 1>{}, act, std::false_type{});
+        if (k + 2 >= n_main) break;
+        tile(k + 2, std::integral_constant<int, 2>{}, act, std::false_type{});
+        if (k + 3 >= n_main) break;
+        tile(k + 3, std::integral_constant<int, 3>{}, act, std::false_type{});
+      }
+    };
+    if (wave_active) tiles(std::true_type{});
+    else tiles(std::false_type{});
     __builtin_amdgcn_s_setprio(0);
     asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
     __syncthreads();  // every wave is done with the rings before the tail reuses them
