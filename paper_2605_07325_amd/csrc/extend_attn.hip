@@ -431,17 +431,19 @@ __global__ void __launch_bounds__(NW * 64, 8 / NW) attn_bf16_kernel(const AttnAr
     const int pidx = t >> log2P;
     return bt ? bt[pidx] : bt_base + pidx;
   };
-  // The same for a key known to lie inside the table row (t < L + n): no
-  // test, and the contiguous cache (no table) by a select, not a branch (the
-  // row's first entry is read instead, and discarded).
+  // The same for a key known to lie inside the table row (t < L + n), with no
+  // test or branch: the table entry is loaded (for the contiguous cache, with
+  // no table, some valid word instead) into `raw` and the contiguous cache's
+  // page id goes to `alt`; page_pick chooses once the load has landed.
   const_i32p bt_row = bt ? bt : (const_i32p)a.cu_q;
   const int bt_any = bt ? -1 : 0;
-
-  auto page_id_in_row = [&](int tile, int g) -> int {
+  auto page_id_in_row = [&](int tile, int g, int& raw, int& alt) {
     const int pidx = block_key(tile, g) >> log2P;
-    const int v = bt_row[pidx & bt_any];
-    return bt_any ? v : bt_base + pidx;
+    // volatile: loaded whether or not a table is present, so no branch appears
+    raw = *(const volatile __attribute__((address_space(4))) int32_t*)(bt_row + (pidx & bt_any));
+    alt = bt_base + pidx;
   };
+  auto page_pick = [&](int raw, int alt) -> int { return bt_any ? raw : alt; };
   auto page_off = [&](int tile, int g, int pg) -> int64_t {
     const int t = block_key(tile, g);
     pg = (uint32_t)pg < (uint32_t)num_pages ? pg : 0;
@@ -722,10 +724,10 @@ __global__ void __launch_bounds__(NW * 64, 8 / NW) attn_bf16_kernel(const AttnAr
     }
   };
   // Main-loop check of a block's probabilities instead of its row max: if in
-  // some lane the 16 of them (formed against the current reference) sum past
-  // 2^16, or to NaN, form the block's exact row max, move the reference,
-  // rescale the row sum and recompute the probabilities; alpha then rescales
-  // O (by the caller, outside this branch, so that O keeps its registers).
+  // either lane of a row the 16 of them (formed against the current
+  // reference) sum past 2^16, or to NaN, form the block's exact row max, move
+  // the reference, rescale the row sum and recompute the probabilities;
+  // alpha then rescales O.
   // Every probability used stays below 2^16, and as with the lazily moved
   // maximum the final normalisation is exact whatever reference was used.
   auto reexp = [&](const f32x16& s, u32x4* pf, float& bsum, float& alpha) {
@@ -743,13 +745,16 @@ __global__ void __launch_bounds__(NW * 64, 8 / NW) attn_bf16_kernel(const AttnAr
     pf[1] = exp_half(s, 1, b1);
     bsum = b0 + b1;
   };
-  // One pipelined block step: exponentials of s_cur (block kb of V tile vl)
-  // against the scores of the next block (block kb_next of K tile kl_next).
-  // Each step also issues two DMA blocks (dma_a, dma_b), one after each half
-  // of the score MFMAs, so each wave's loads trickle into the memory pipeline
-  // instead of arriving with every other wave's at the tile boundary.
-  // K fragments of the first half of the next step's score block, read one
-  // group of products ahead so that their LDS latency hides behind MFMAs.
+  // One pipelined block step: the probabilities of s_cur (block kb of V tile
+  // vl) are formed while the MFMA pipe works on the scores of the next block
+  // (block kb_next of K tile kl_next); then the block's check, the next K
+  // fragments' reads and P V.  dma_a / dma_b issue this wave's DMA runs of
+  // the step (one tensor per step) and, after the second step's, the page
+  // ids of the tile after next.  The compiler schedules the step freely; the
+  // empty asm markers (pin) keep each half's probabilities next to the score
+  // products they overlap.  K fragments of the first half of the next step's
+  // score block are read one group of products ahead, so that their LDS
+  // latency hides behind MFMAs.
   KF kpre[DS / 2];
   auto step = [&](f32x16& s_cur, f32x16& s_next, auto voff_c, const char* kl_next, int kb_next,
                   const char* kl_after, int kb_after, auto dma_a, auto dma_b) {
@@ -758,30 +763,30 @@ __global__ void __launch_bounds__(NW * 64, 8 / NW) attn_bf16_kernel(const AttnAr
     float b0, b1;
     s_next = f32x16{};
     load_k(kl_next, kb_next, DS / 2, kh1);
-    __builtin_amdgcn_sched_barrier(0);
     pf[0] = exp_half(s_cur, 0, b0);
     mfma_k(kpre, 0, s_next);
     pin(pf[0]);
-    __builtin_amdgcn_sched_barrier(0);
     dma_a();
-    __builtin_amdgcn_sched_barrier(0);
     pf[1] = exp_half(s_cur, 1, b1);
     mfma_k(kh1, DS / 2, s_next);
     pin(pf[1]);
-    __builtin_amdgcn_sched_barrier(0);
-    float bsum = b0 + b1, alpha = 1.f;
-    const bool redo = __any(!(bsum <= 65536.f));
-    if (redo) reexp(s_cur, pf, bsum, alpha);
-    lrow += bsum;
-    __builtin_amdgcn_sched_barrier(0);
-    dma_b();
-    __builtin_amdgcn_sched_barrier(0);
-    load_k(kl_after, kb_after, 0, kpre);
-    __builtin_amdgcn_sched_barrier(0);
-    if (redo) {
+    float bsum = b0 + b1;
+    {
+      // Per row (lanes l and l^32 hold its two halves), as a divergent
+      // branch: the rare path then writes the fast path's registers under
+      // the exec mask instead of leaving copies on the fast path.
+      const uint32_t ov = !(bsum <= 65536.f) ? 1u : 0u;
+      const auto pr = __builtin_amdgcn_permlane32_swap(ov, ov, false, false);
+      if ((pr[0] | pr[1]) != 0u) {
+        float alpha;
+        reexp(s_cur, pf, bsum, alpha);
 #pragma unroll
-      for (int db = 0; db < DB; ++db) o[db] *= alpha;
+        for (int db = 0; db < DB; ++db) o[db] *= alpha;
+      }
     }
+    lrow += bsum;
+    dma_b();
+    load_k(kl_after, kb_after, 0, kpre);
     pv_asm(voff_c, pf);
     s_cur = s_next;
   };
@@ -797,7 +802,8 @@ __global__ void __launch_bounds__(NW * 64, 8 / NW) attn_bf16_kernel(const AttnAr
     // previous tile's loads" is the constant vmcnt(2*NDMA).
     auto clampt = [&](int t) { return min(t, main_end - 1); };
     int64_t pgn[NPG];  // page offsets of tile tb+k+3, issued at tile k
-    int pgi[NPG];      // their raw page ids, loaded half a tile earlier
+    int pgi[NPG];      // their page ids (raw table words), loaded half a tile earlier
+    int pga[NPG];      // ... and the contiguous cache's ids (used when there is no table)
     {
       int64_t pg[NPG];
       if (dma_wave) {
@@ -810,7 +816,7 @@ __global__ void __launch_bounds__(NW * 64, 8 / NW) attn_bf16_kernel(const AttnAr
         }
       }
 #pragma unroll
-      for (int g = 0; g < NPG; ++g) pgi[g] = dma_wave ? page_id(clampt(u.tb + 3), g) : 0;
+      for (int g = 0; g < NPG; ++g) pgi[g] = pga[g] = dma_wave ? page_id(clampt(u.tb + 3), g) : 0;
     }
     asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
     __syncthreads();
@@ -828,9 +834,21 @@ __global__ void __launch_bounds__(NW * 64, 8 / NW) attn_bf16_kernel(const AttnAr
     // PFX: the tile whose DMA this tile issues (tb+k+3) lies wholly in the
     // cached prefix, so is the one whose page id it loads (tb+k+4) inside the
     // table row: neither needs a test.
-    auto tile = [&](int k, auto stage, auto act, auto pfx) {
+    // CLS: 1 / 2 when the caller knows the wave is in the lower / upper half
+    // (its issue-priority turns then need no branch), 0 otherwise.
+    auto tile = [&](int k, auto stage, auto act, auto pfx, auto cls) {
       constexpr int S = decltype(stage)::value;
       constexpr bool ACT = decltype(act)::value;
+      constexpr int CLS = decltype(cls)::value;
+      auto prio = [&](bool first) {
+        if constexpr (CLS == 1) {
+          if (first) __builtin_amdgcn_s_setprio(1); else __builtin_amdgcn_s_setprio(0);
+        } else if constexpr (CLS == 2) {
+          if (first) __builtin_amdgcn_s_setprio(0); else __builtin_amdgcn_s_setprio(1);
+        } else {
+          if ((wave < NW / 2) == first) __builtin_amdgcn_s_setprio(1); else __builtin_amdgcn_s_setprio(0);
+        }
+      };
       // Tiles k and k+1 have landed in LDS (only the previous tile's DMA may
       // still be in flight) and this wave's LDS reads of tile k-1 are done.
       // A plain s_barrier: __syncthreads() would also fence, i.e. wait for the
@@ -852,7 +870,7 @@ __global__ void __launch_bounds__(NW * 64, 8 / NW) attn_bf16_kernel(const AttnAr
       const int nt = clampt(u.tb + k + 3);
       if (dma_wave) {
 #pragma unroll
-        for (int g = 0; g < NPG; ++g) pgn[g] = page_off(nt, g, pgi[g]);
+        for (int g = 0; g < NPG; ++g) pgn[g] = page_off(nt, g, page_pick(pgi[g], pga[g]));
       }
       char* kdst = kring + ((S + 3) % ST) * TILEB;
       char* vdst = vring + ((S + 3) % ST) * TILEB;
@@ -878,20 +896,20 @@ __global__ void __launch_bounds__(NW * 64, 8 / NW) attn_bf16_kernel(const AttnAr
         for (int g = NG0; g < NPG; ++g) issue_group(nt, g, pgn[g], vdst, vpool, vnew, pfx);
 #pragma unroll
         for (int g = 0; g < NPG; ++g) {
-          if constexpr (SCALAR_PAGES && decltype(pfx)::value) pgi[g] = page_id_in_row(clampt(u.tb + k + 4), g);
-          else pgi[g] = page_id(clampt(u.tb + k + 4), g);
+          if constexpr (SCALAR_PAGES && decltype(pfx)::value) page_id_in_row(clampt(u.tb + k + 4), g, pgi[g], pga[g]);
+          else pgi[g] = pga[g] = page_id(clampt(u.tb + k + 4), g);
         }
       };
       // The two waves of a SIMD take turns at the higher issue priority, one
       // step each, so that neither lags the other into the tile barrier.
-      if (wave < NW / 2) __builtin_amdgcn_s_setprio(1); else __builtin_amdgcn_s_setprio(0);
+      prio(true);
       // block 0 || scores of block 1, then block 1 || scores of the next tile's block 0
       if constexpr (!ACT) {
         kd0(); kd1(); vd0(); vd1();
         return;
       }
       step(s_a, s_b, std::integral_constant<int, S * TILEB>{}, kl, 1, kring + ((S + 1) % ST) * TILEB, 0, kd0, kd1);
-      if (wave < NW / 2) __builtin_amdgcn_s_setprio(0); else __builtin_amdgcn_s_setprio(1);
+      prio(false);
       step(s_a, s_b, std::integral_constant<int, S * TILEB + 32 * ROWB>{}, kring + ((S + 1) % ST) * TILEB, 0,
            kring + ((S + 1) % ST) * TILEB, 1, vd0, vd1);
     };
@@ -900,24 +918,33 @@ __global__ void __launch_bounds__(NW * 64, 8 / NW) attn_bf16_kernel(const AttnAr
     // per-tile classification; the rest take the general path.
     const int pfx_tiles = u.L / KT;  // tiles [0, pfx_tiles) are wholly cached
     const int k_pfx = main_end - 1 < pfx_tiles ? n_main : max(0, min(n_main, pfx_tiles - u.tb - 3));
+    auto prefix_tiles = [&](int& k, auto act, auto cls) {
+      for (; k + 4 <= k_pfx; k += 4) {
+        tile(k, std::integral_constant<int, 0>{}, act, std::true_type{}, cls);
+        tile(k + 1, std::integral_constant<int, 1>{}, act, std::true_type{}, cls);
+        tile(k + 2, std::integral_constant<int, 2>{}, act, std::true_type{}, cls);
+        tile(k + 3, std::integral_constant<int, 3>{}, act, std::true_type{}, cls);
+      }
+    };
     auto tiles = [&](auto act) {
       int k = 0;
       if constexpr (SCALAR_PAGES) {
-        for (; k + 4 <= k_pfx; k += 4) {
-          tile(k, std::integral_constant<int, 0>{}, act, std::true_type{});
-          tile(k + 1, std::integral_constant<int, 1>{}, act, std::true_type{});
-          tile(k + 2, std::integral_constant<int, 2>{}, act, std::true_type{});
-          tile(k + 3, std::integral_constant<int, 3>{}, act, std::true_type{});
+        // computing waves: one copy of the loop per half, for branch-free priority turns
+        if constexpr (decltype(act)::value) {
+          if (wave < NW / 2) prefix_tiles(k, act, std::integral_constant<int, 1>{});
+          else prefix_tiles(k, act, std::integral_constant<int, 2>{});
+        } else {
+          prefix_tiles(k, act, std::integral_constant<int, 0>{});
         }
       }
       for (; k < n_main; k += 4) {
-        tile(k, std::integral_constant<int, 0>{}, act, std::false_type{});
+        tile(k, std::integral_constant<int, 0>{}, act, std::false_type{}, std::integral_constant<int, 0>{});
         if (k + 1 >= n_main) break;
-        tile(k + 1, std::integral_constant<int, 1>{}, act, std::false_type{});
+        tile(k + 1, std::integral_constant<int, 1>{}, act, std::false_type{}, std::integral_constant<int, 0>{});
         if (k + 2 >= n_main) break;
-        tile(k + 2, std::integral_constant<int, 2>{}, act, std::false_type{});
+        tile(k + 2, std::integral_constant<int, 2>{}, act, std::false_type{}, std::integral_constant<int, 0>{});
         if (k + 3 >= n_main) break;
-        tile(k + 3, std::integral_constant<int, 3>{}, act, std::false_type{});
+        tile(k + 3, std::integral_constant<int, 3>{}, act, std::false_type{}, std::integral_constant<int, 0>{});
       }
     };
     if (wave_active) tiles(std::true_type{});
