@@ -431,19 +431,34 @@ __global__ void __launch_bounds__(NW * 64, 8 / NW) attn_bf16_kernel(const AttnAr
     const int pidx = t >> log2P;
     return bt ? bt[pidx] : bt_base + pidx;
   };
-  // The same for a key known to lie inside the table row (t < L + n), with no
-  // test or branch: the table entry is loaded (for the contiguous cache, with
-  // no table, some valid word instead) into `raw` and the contiguous cache's
-  // page id goes to `alt`; page_pick chooses once the load has landed.
+  // Page ids of the prefix loop, with no test or branch: the table entry is
+  // loaded (for the contiguous cache, with no table, the first word of
+  // cu_seqlens instead) into `raw` and the contiguous cache's page id goes
+  // to `alt`; page_pick chooses once the load has landed.
   const_i32p bt_row = bt ? bt : (const_i32p)a.cu_q;
   const int bt_any = bt ? -1 : 0;
-  auto page_id_in_row = [&](int tile, int g, int& raw, int& alt) {
-    const int pidx = block_key(tile, g) >> log2P;
-    // volatile: loaded whether or not a table is present, so no branch appears
-    raw = *(const volatile __attribute__((address_space(4))) int32_t*)(bt_row + (pidx & bt_any));
+  auto page_pick = [&](int raw, int alt) -> int { return bt_any ? raw : alt; };
+  // Prefix loop (pages of at most 64 keys, so a tile starts a page): the page
+  // index of lookup group g of tile t is (t << pidx_sh) + pidx_g[g], clamped
+  // to the row's last page; the page's byte offset is a 32 x 32-bit product.
+  const int pidx_sh = log2P <= 6 ? 6 - log2P : 0;
+  const int last_pidx = last_key >> log2P;
+  const uint32_t page_bytes32 = (uint32_t)page_bytes;
+  int pidx_g[NPG];
+#pragma unroll
+  for (int g = 0; g < NPG; ++g) pidx_g[g] = SCALAR_PAGES ? (blk(g * PB) * ROWS_PER_KB) >> log2P : 0;
+  // The load is inline assembly (a scalar load with a register byte offset):
+  // it is issued whether or not a table is present, and its result is only
+  // read after the tile-start wait, which covers it.
+  auto page_id_pfx = [&](int tile, int g, int& raw, int& alt) {
+    const int pidx = min((tile << pidx_sh) + pidx_g[g], last_pidx);
+    const uint32_t off = (uint32_t)(pidx & bt_any) << 2;
+    asm volatile("s_load_dword %0, %1, %2" : "=s"(raw) : "s"(bt_row), "s"(off));
     alt = bt_base + pidx;
   };
-  auto page_pick = [&](int raw, int alt) -> int { return bt_any ? raw : alt; };
+  auto page_off_pfx = [&](int pg) -> int64_t {
+    return (int64_t)((uint64_t)((uint32_t)pg < (uint32_t)num_pages ? (uint32_t)pg : 0u) * page_bytes32);
+  };
   auto page_off = [&](int tile, int g, int pg) -> int64_t {
     const int t = block_key(tile, g);
     pg = (uint32_t)pg < (uint32_t)num_pages ? pg : 0;
@@ -870,7 +885,10 @@ __global__ void __launch_bounds__(NW * 64, 8 / NW) attn_bf16_kernel(const AttnAr
       const int nt = clampt(u.tb + k + 3);
       if (dma_wave) {
 #pragma unroll
-        for (int g = 0; g < NPG; ++g) pgn[g] = page_off(nt, g, page_pick(pgi[g], pga[g]));
+        for (int g = 0; g < NPG; ++g) {
+          if constexpr (SCALAR_PAGES && decltype(pfx)::value) pgn[g] = page_off_pfx(page_pick(pgi[g], pga[g]));
+          else pgn[g] = page_off(nt, g, page_pick(pgi[g], pga[g]));
+        }
       }
       char* kdst = kring + ((S + 3) % ST) * TILEB;
       char* vdst = vring + ((S + 3) % ST) * TILEB;
@@ -896,7 +914,7 @@ __global__ void __launch_bounds__(NW * 64, 8 / NW) attn_bf16_kernel(const AttnAr
         for (int g = NG0; g < NPG; ++g) issue_group(nt, g, pgn[g], vdst, vpool, vnew, pfx);
 #pragma unroll
         for (int g = 0; g < NPG; ++g) {
-          if constexpr (SCALAR_PAGES && decltype(pfx)::value) page_id_in_row(clampt(u.tb + k + 4), g, pgi[g], pga[g]);
+          if constexpr (SCALAR_PAGES && decltype(pfx)::value) page_id_pfx(u.tb + k + 4, g, pgi[g], pga[g]);
           else pgi[g] = pga[g] = page_id(clampt(u.tb + k + 4), g);
         }
       };
@@ -917,7 +935,7 @@ __global__ void __launch_bounds__(NW * 64, 8 / NW) attn_bf16_kernel(const AttnAr
     // cached prefix run first, in whole rounds of the ring, without the
     // per-tile classification; the rest take the general path.
     const int pfx_tiles = u.L / KT;  // tiles [0, pfx_tiles) are wholly cached
-    const int k_pfx = main_end - 1 < pfx_tiles ? n_main : max(0, min(n_main, pfx_tiles - u.tb - 3));
+    const int k_pfx = log2P > 6 ? 0 : main_end - 1 < pfx_tiles ? n_main : max(0, min(n_main, pfx_tiles - u.tb - 3));
     auto prefix_tiles = [&](int& k, auto act, auto cls) {
       for (; k + 4 <= k_pfx; k += 4) {
         tile(k, std::integral_constant<int, 0>{}, act, std::true_type{}, cls);
