@@ -207,6 +207,32 @@ csr_status csr_extend_attention(const csr_attn_desc* desc, int32_t batch, const 
                                 uint32_t flags, void* out, float* lse, void* workspace,
                                 size_t workspace_bytes, void* stream);
 
+/*
+ * For callers that cannot allocate device memory (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid hipMalloc): the same
+ * operation as csr_extend_attention, with the same arguments except the
+ * workspace.  The workspace lives in a scratch array of
+ * CSR_NOALLOC_SCRATCH_BYTES that the library's code object holds on each
+ * device it runs on, for as long as the process lives; the call allocates and
+ * frees nothing.  Calls whose csr_extend_workspace_size exceeds that size
+ * return CSR_E_WORKSPACE.  Every call on a device shares that device's array
+ * (which keeps the last call's contents; nothing in it needs clearing), so
+ * calls that overlap on one device - on different streams, or from different
+ * threads without ordering - race and give undefined results.  On its first
+ * call on a device (with that device current) the entry point looks the
+ * array's address up with hipGetSymbolAddress, a HIP runtime call made before
+ * the argument checks end; otherwise as csr_extend_attention.
+ */
+#define CSR_NOALLOC_SCRATCH_BYTES (64u << 20)
+csr_status csr_extend_attention_noalloc(const csr_attn_desc* desc, int32_t batch, const void* q,
+                                        const void* k_new, const void* v_new, void* k_pool,
+                                        void* v_pool, int32_t num_pages,
+                                        const int32_t* block_table, int32_t bt_stride,
+                                        const int32_t* cu_seqlens_q, const int32_t* cache_seqlens,
+                                        int32_t total_q, int32_t max_seqlen_q,
+                                        int32_t max_cache_len, uint32_t flags, void* out,
+                                        float* lse, void* stream);
+
 /* Workspace bytes csr_prefill needs (split-K partials, rotated q/k with RoPE; 0 if neither). */
 size_t csr_prefill_workspace_size(const csr_attn_desc* desc, int32_t batch, int32_t total,
                                   int32_t max_seqlen);

@@ -22,11 +22,12 @@ CSR_F32, CSR_BF16 = 0, 1
 CSR_APPEND = 1
 CSR_ROPE_NONE, CSR_ROPE_NEOX, CSR_ROPE_INTERLEAVED = 0, 1, 2
 CSR_KV_SAME, CSR_KV_FP8_E4M3 = 0, 1
+CSR_NOALLOC_SCRATCH_BYTES = 64 << 20  # include/csr.h
 
 # Every function include/csr.h declares.
 EXPORTS = ("csr_kv_append", "csr_extend_workspace_size", "csr_extend_attention", "csr_prefill_workspace_size",
-           "csr_prefill", "csr_set_attention_events", "csr_set_plan_overrides", "csr_status_string",
-           "csr_last_error")
+           "csr_extend_attention_noalloc", "csr_prefill", "csr_set_attention_events", "csr_set_plan_overrides",
+           "csr_status_string", "csr_last_error")
 
 
 class AttnDesc(ctypes.Structure):
@@ -60,6 +61,9 @@ def lib() -> ctypes.CDLL:
         L.csr_extend_workspace_size.restype = sz
         L.csr_extend_attention.argtypes = [D, i32, p, p, p, p, p, i32, p, i32, p, p, i32, i32, i32, u32, p, p, p, sz, p]
         L.csr_extend_attention.restype = ctypes.c_int
+        L.csr_extend_attention_noalloc.argtypes = [D, i32, p, p, p, p, p, i32, p, i32, p, p, i32, i32, i32, u32, p, p,
+                                                   p]
+        L.csr_extend_attention_noalloc.restype = ctypes.c_int
         L.csr_prefill_workspace_size.argtypes = [D, i32, i32, i32]
         L.csr_prefill_workspace_size.restype = sz
         L.csr_prefill.argtypes = [D, i32, p, p, p, p, p, i32, p, i32, p, i32, i32, p, p, p, sz, p]
@@ -204,6 +208,24 @@ def extend_attention(desc: AttnDesc, q, k_new, v_new, k_pool, v_pool, block_tabl
         ctypes.byref(desc), batch, _ptr(q), _ptr(k_new), _ptr(v_new), _ptr(k_pool), _ptr(v_pool), _pool_pages(desc, k_pool, v_pool),
         _ptr(block_table), bt_stride, _ptr(cu_seqlens_q), _ptr(cache_seqlens), total_q, max_seqlen_q, max_cache_len,
         CSR_APPEND if append else 0, _ptr(out), _ptr(lse), _ptr(workspace), ws_cap, _stream(stream)))
+    return out, lse
+
+
+def extend_attention_noalloc(desc: AttnDesc, q, k_new, v_new, k_pool, v_pool, block_table, bt_stride: int,
+                             cu_seqlens_q, cache_seqlens, max_seqlen_q: int, max_cache_len: int, append: bool = False,
+                             out=None, lse: Optional[torch.Tensor] = None, want_lse: bool = True, stream=None):
+    """csr_extend_attention_noalloc: as ``extend_attention`` with the library's own scratch array as the
+    workspace (the binding still allocates ``out`` / ``lse`` when they are not supplied)."""
+    batch = int(cu_seqlens_q.shape[0]) - 1
+    total_q = int(q.shape[0])
+    if out is None:
+        out = torch.empty_like(q)
+    if lse is None and want_lse:
+        lse = torch.empty((total_q, desc.num_q_heads), dtype=torch.float32, device=q.device)
+    _check(lib().csr_extend_attention_noalloc(
+        ctypes.byref(desc), batch, _ptr(q), _ptr(k_new), _ptr(v_new), _ptr(k_pool), _ptr(v_pool),
+        _pool_pages(desc, k_pool, v_pool), _ptr(block_table), bt_stride, _ptr(cu_seqlens_q), _ptr(cache_seqlens), total_q,
+        max_seqlen_q, max_cache_len, CSR_APPEND if append else 0, _ptr(out), _ptr(lse), _stream(stream)))
     return out, lse
 
 

@@ -11,6 +11,7 @@
 #include <stdlib.h>
 
 #include <atomic>
+#include <mutex>
 #include <string>
 
 #include "../../include/csr.h"
@@ -405,6 +406,37 @@ csr_status run_attention(const csr_attn_desc* d, int batch, const void* q, const
   return launched(csr::launch_merge(m, d->dtype == CSR_BF16, stream), "split-K merge");
 }
 
+
+// ---- Scratch of csr_extend_attention_noalloc: one array per device, in the
+// library's code object, holding what the workspace holds for
+// csr_extend_attention.  Host code reaches it only through the address
+// hipGetSymbolAddress returns for the current device (the array's name in
+// host code is a host-side stand-in, not a device address).
+constexpr size_t kNoAllocScratchBytes = (size_t)CSR_NOALLOC_SCRATCH_BYTES;
+static __device__ __align__(256) char scratch[kNoAllocScratchBytes];
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kMaxDevices];
+
+// Device address of `scratch` on the current device, looked up on the first
+// call for that device (with the device current) and kept for the process.
+csr_status scratch_of_current_device(void** out) {
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return fail(CSR_E_HIP, "hipGetDevice failed: %s", hipGetErrorString(e));
+  if (dev < 0 || dev >= kMaxDevices) return fail(CSR_E_UNSUPPORTED, "device %d beyond the %d the library tracks", dev,
+                                                 kMaxDevices);
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    void* ptr = nullptr;
+    e = hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch));
+    if (e != hipSuccess || !ptr)
+      return fail(CSR_E_HIP, "hipGetSymbolAddress(scratch) on device %d failed: %s", dev, hipGetErrorString(e));
+    g_scratch_ptr[dev] = ptr;
+  }
+  *out = g_scratch_ptr[dev];
+  return CSR_OK;
+}
+
 }  // namespace
 
 extern "C" {
@@ -536,6 +568,27 @@ csr_status csr_extend_attention(const csr_attn_desc* desc, int32_t batch, const 
   return run_attention(desc, batch, q, k_new, v_new, k_pool, v_pool, num_pages, block_table, bt_stride, cu_seqlens_q,
                        max_cache_len > 0 ? cache_seqlens : nullptr, total_q, max_seqlen_q, max_cache_len, out, lse,
                        workspace, workspace_bytes, s, append ? &app : nullptr);
+}
+
+csr_status csr_extend_attention_noalloc(const csr_attn_desc* desc, int32_t batch, const void* q, const void* k_new,
+                                        const void* v_new, void* k_pool, void* v_pool, int32_t num_pages,
+                                        const int32_t* block_table, int32_t bt_stride, const int32_t* cu_seqlens_q,
+                                        const int32_t* cache_seqlens, int32_t total_q, int32_t max_seqlen_q,
+                                        int32_t max_cache_len, uint32_t flags, void* out, float* lse, void* stream) {
+  g_last_error.clear();
+  const size_t need =
+      total_q > 0 ? csr_extend_workspace_size(desc, batch, total_q, max_seqlen_q, max_cache_len) : (size_t)0;
+  if (need > kNoAllocScratchBytes)
+    return fail(CSR_E_WORKSPACE, "this call needs %zu bytes of scratch; the no-allocation entry point has %zu",
+                need, kNoAllocScratchBytes);
+  void* ws = nullptr;
+  if (need > 0) {
+    const csr_status st = scratch_of_current_device(&ws);
+    if (st != CSR_OK) return st;
+  }
+  return csr_extend_attention(desc, batch, q, k_new, v_new, k_pool, v_pool, num_pages, block_table, bt_stride,
+                              cu_seqlens_q, cache_seqlens, total_q, max_seqlen_q, max_cache_len, flags, out, lse, ws,
+                              need > 0 ? kNoAllocScratchBytes : 0, stream);
 }
 
 csr_status csr_prefill(const csr_attn_desc* desc, int32_t batch, const void* q, const void* k, const void* v,
