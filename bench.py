@@ -23,6 +23,13 @@ steps the difference is visible, for the 512-token chunk it is below 1 %.
 inside the step (one fused rotate-and-append launch before the attention) and
 reports the hook-free step time with and without the rotation.
 
+With the default workload the line also carries ``sweep``: the other
+workloads (one-token decode over the 120K prefix with a bf16 and an e4m3
+cache, n = 64 / 128 / 1024, the 8K-prefix chunk, the ragged batch of eight,
+the 61440-token re-prefill), each with its attention-kernel median and minimum,
+its step time and the kernel against its own roofline.  ``step_ms_stats`` and
+``kernel_ms_median`` / ``kernel_ms_min`` give the spread of the headline steps.
+
 Prints one JSON line.  ``--gpus N`` with N > 1 is rejected: the benchmark
 measures one GPU (the attention shards without communication by kv head and
 by sequence; that split is not run here).
@@ -149,6 +156,126 @@ def cpu_baseline(case, target_s: float):
     return {"value": tflops, "unit": "TFLOP/s", "cores": threads, "kind": "oracle",
             "sample": (f"{cnt} of {case.total_q} query tokens, all {case.num_q_heads} heads, of the same workload "
                        f"({fl / 1e9:.1f} GFLOP, {dt:.1f} s; full layer extrapolates to {full_s:.0f} s)")}
+
+
+SWEEP_DEFAULT = "c3_1,c3_1_fp8,c3_64,c3_128,c3_1024,c2,c5,c4_61440"
+
+
+def run_sweep(args, torch, csr, dg, names):
+    """The other workloads, one compact record each: attention-kernel time
+    (median and min over the timed steps, through the library's event hook),
+    the step time of the whole path without the hook, and the kernel against
+    its own roofline (HBM for the one-token decode steps, MFMA otherwise).
+    Values are drawn on the device (i.i.d. normal x 0.5 rounded to bf16, or
+    random e4m3 codes) in the layout the seeded generator draws (lengths, page
+    table), which keeps the sweep to seconds."""
+    out = {"kernel_sha": kernel_source_hash(), "configs": []}
+    gen = torch.Generator(device="cuda")
+    for name in [x for x in names.split(",") if x]:
+        fp8 = name.endswith("_fp8")
+        cfg = name[:-4] if fp8 else name
+        case = dg.config(cfg, fill=False)
+        prefill_mode = int(case.cache_len.max()) == 0
+        gen.manual_seed(1000 + len(out["configs"]))
+
+        def normal(shape):
+            return (torch.randn(shape, generator=gen, device="cuda") * 0.5).to(torch.bfloat16)
+
+        def codes(shape):  # e4m3 patterns: random sign and mantissa, exponent field 3..9 (never NaN)
+            sgn = torch.randint(0, 2, shape, generator=gen, device="cuda", dtype=torch.uint8) << 7
+            exp = torch.randint(3, 10, shape, generator=gen, device="cuda", dtype=torch.uint8) << 3
+            man = torch.randint(0, 8, shape, generator=gen, device="cuda", dtype=torch.uint8)
+            return sgn | exp | man
+
+        q, k_new, v_new = normal(case.q.shape), normal(case.k_new.shape), normal(case.v_new.shape)
+        mk = codes if fp8 else normal
+        pools = [(mk(case.k_pool.shape), mk(case.v_pool.shape)) for _ in range(max(1, args.pools))]
+        bt = None if case.block_table is None else torch.from_numpy(case.block_table).cuda()
+        cu = torch.from_numpy(case.cu_seqlens_q).cuda()
+        cl = torch.from_numpy(case.cache_len).cuda()
+        desc = csr.make_desc(case.num_q_heads, case.num_kv_heads, case.head_dim, case.page_size, torch.bfloat16,
+                             kv_dtype=csr.CSR_KV_FP8_E4M3 if fp8 else csr.CSR_KV_SAME,
+                             k_scale=0.0625 if fp8 else 0.0, v_scale=0.0390625 if fp8 else 0.0)
+        o = torch.empty_like(q)
+        lse = torch.empty((case.total_q, case.num_q_heads), dtype=torch.float32, device="cuda")
+        if prefill_mode:
+            wsb = csr.prefill_workspace_size(desc, case.batch, case.total_q, case.max_seqlen_q)
+        else:
+            wsb = csr.extend_workspace_size(desc, case.batch, case.total_q, case.max_seqlen_q, case.max_cache_len)
+        ws = torch.empty(max(wsb, 16), dtype=torch.uint8, device="cuda")
+
+        def step(i):
+            kp, vp = pools[i % len(pools)]
+            if prefill_mode:
+                csr.prefill(desc, q, k_new, v_new, cu, case.max_seqlen_q, k_pool=kp, v_pool=vp, block_table=bt,
+                            bt_stride=case.bt_stride, out=o, lse=lse, workspace=ws)
+            else:
+                csr.extend_attention(desc, q, k_new, v_new, kp, vp, bt, case.bt_stride, cu, cl, case.max_seqlen_q,
+                                     case.max_cache_len, append=True, out=o, lse=lse, workspace=ws)
+
+        flops = case.flops()
+        steps = max(5, min(args.steps, int(2000.0 / max(1.0, flops / 1.2e12))))  # about 2 s of work at most
+        for i in range(5):
+            step(i)
+        torch.cuda.synchronize()
+        s0, e0 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        s0.record()
+        for i in range(steps):
+            step(i)
+        e0.record()
+        torch.cuda.synchronize()
+        step_ms = s0.elapsed_time(e0) / steps
+        kms = hooked_kernel_ms(torch, csr, step, steps)
+        kmed = float(np.median(kms))
+        abytes = case.algorithmic_bytes(append=True, kv_bytes=1 if fp8 else None)
+        hbm = case.max_seqlen_q == 1
+        if hbm:
+            ach, peak, unit = abytes / (kmed * 1e-3) / 1e9, PEAK_HBM_GBS, "GB/s"
+        else:
+            ach, peak, unit = flops / (kmed * 1e-3) / 1e12, PEAK_BF16_TFLOPS, "TFLOP/s"
+        ent = {
+            "name": name,
+            "workload": (f"{'re-prefill' if prefill_mode else 'extend'}: L={case.cache_len.tolist() if case.batch > 1 else case.max_cache_len} "
+                         f"n={case.seqlen_q.tolist() if case.batch > 1 else case.max_seqlen_q}"
+                         + (", fp8 e4m3 cache" if fp8 else "")),
+            "kernel_ms_median": round(kmed, 5),
+            "kernel_ms_min": round(float(np.min(kms)), 5),
+            "step_ms": round(step_ms, 5),
+            "steps": steps,
+            "bound": "hbm" if hbm else "mfma",
+            "achieved": round(ach, 1),
+            "peak": peak,
+            "unit": unit,
+            "frac": round(ach / peak, 4),
+            "traffic": measured_traffic(name),
+        }
+        if hbm:
+            ent["step_gbs"] = round(abytes / (step_ms * 1e-3) / 1e9, 1)
+        else:
+            ent["tflops_step"] = round(flops / (step_ms * 1e-3) / 1e12, 1)
+        out["configs"].append(ent)
+        log(f"sweep {name}: kernel {kmed:.4f} ms (min {ent['kernel_ms_min']:.4f}), step {step_ms:.4f} ms, "
+            f"{ach:.1f} {unit} = {100 * ach / peak:.1f}% of {peak:g}")
+        del q, k_new, v_new, pools, o, lse, ws
+        torch.cuda.empty_cache()
+    return out
+
+
+def hooked_kernel_ms(torch, csr, step, steps):
+    """Attention-kernel durations of ``steps`` steps through the event hook."""
+    hip = HipEvents()
+    evs = [(hip.create(), hip.create()) for _ in range(steps)]
+    torch.cuda.synchronize()
+    for i in range(steps):
+        csr.set_attention_events(*evs[i])
+        step(i)
+    csr.set_attention_events(None, None)
+    torch.cuda.synchronize()
+    ms = [hip.elapsed_ms(a, b) for a, b in evs]
+    for a, b in evs:
+        hip.destroy(a)
+        hip.destroy(b)
+    return ms
 
 
 def run_asr(args, torch, csr):
@@ -329,6 +456,9 @@ def main():
     ap.add_argument("--asr-dump", default="", help="asr: directory for per-task latency arrays")
     ap.add_argument("--asr-modes", default="steady,blocking,asr,asr_partitioned,asr_shared",
                     help="asr: runs to make (the JSON value is the 'asr' run's p99)")
+    ap.add_argument("--sweep", default="auto",
+                    help="comma-separated workloads for the compact 'sweep' record ('' to skip; a _fp8 suffix "
+                         f"selects the e4m3 cache); 'auto' = {SWEEP_DEFAULT} with the default workload, none otherwise")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="also run a 1 GiB device copy (HBM counter calibration for rocprofv3 --pmc runs)")
     args = ap.parse_args()
@@ -512,6 +642,22 @@ def main():
     plain_ms = hookless_ms(desc)
     rec["ms_per_step_without_event_hook"] = round(plain_ms, 5)
     log(f"same steps without the attention event hook: {plain_ms:.4f} ms/step")
+    # Spread of the step: one event pair around each step (a separate pass; the
+    # value above comes from the two events around all K steps).
+    sev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(args.steps)]
+    for i, (a, b) in enumerate(sev):
+        a.record()
+        step(args.warmup + i)
+        b.record()
+    torch.cuda.synchronize()
+    sms = [a.elapsed_time(b) for a, b in sev]
+    rec["step_ms_stats"] = {"mean": round(ms_per_step, 5), "median": round(float(np.median(sms)), 5),
+                            "min": round(float(np.min(sms)), 5), "per_step_pass_mean": round(float(np.mean(sms)), 5)}
+    rec["roofline"]["kernel_ms_median"] = round(float(np.median(attn_ms)), 5)
+    rec["roofline"]["kernel_ms_min"] = round(float(np.min(attn_ms)), 5)
+    rec["roofline"]["kernel_sha"] = kernel_source_hash()
+    log(f"step median {rec['step_ms_stats']['median']:.4f} ms, min {rec['step_ms_stats']['min']:.4f} ms; kernel "
+        f"median {rec['roofline']['kernel_ms_median']:.4f} ms, min {rec['roofline']['kernel_ms_min']:.4f} ms")
     if bf16:
         mtf, mghz, mms = measured_mfma_peak(torch)
         rec["roofline"]["measured_mfma"] = {
@@ -565,6 +711,13 @@ def main():
         }
         log(f"re-prefill of the same {S}-token history: {pms:.2f} ms ({pms / ms_per_step:.1f}x the extend step)")
         del qq, kk, vv, o2, ws2
+    sweep = args.sweep
+    if sweep == "auto":
+        sweep = SWEEP_DEFAULT if (args.workload == "c3_512" and not fp8 and not rope_style) else ""
+    if sweep:
+        del pools, ws
+        torch.cuda.empty_cache()
+        rec["sweep"] = run_sweep(args, torch, csr, dg, sweep)
     if not args.no_cpu_baseline:
         rec["cpu_baseline"] = cpu_baseline(case, args.cpu_seconds)
     print(json.dumps(rec), flush=True)

@@ -165,7 +165,7 @@ def _place_prefix(pool: np.ndarray, prefix: np.ndarray, table_row: Optional[np.n
 def make_case(name: str, *, dtype: str, num_q_heads: int, num_kv_heads: int, head_dim: int,
               cache_len, seqlen_q, page_size: int = 16, scale: float = 1.0, seed: int = 0,
               cfg_id: int = 0, paged: bool = True, interleave: bool = False,
-              spare_pages: int = 0, keep_prefix: bool = False) -> Case:
+              spare_pages: int = 0, keep_prefix: bool = False, fill: bool = True) -> Case:
     """Build one workload.
 
     ``paged=False`` gives the contiguous cache (identity table: sequence b owns
@@ -173,7 +173,9 @@ def make_case(name: str, *, dtype: str, num_q_heads: int, num_kv_heads: int, hea
     ceil((L_b + n_b) / P) pages; ``interleave`` deals page ids round-robin over
     (page index, sequence) before a seeded permutation of the pool, otherwise
     one seeded permutation is drawn per table.  Slots that hold no prefix token
-    carry a NaN canary.
+    carry a NaN canary.  ``fill=False`` draws the layout only (lengths, page
+    table): the value arrays are then read-only zero-stride views of the right
+    shapes, for callers that draw the values elsewhere.
     """
     L = np.asarray(cache_len, dtype=np.int32).reshape(-1)
     n = np.asarray(seqlen_q, dtype=np.int32).reshape(-1)
@@ -208,6 +210,12 @@ def make_case(name: str, *, dtype: str, num_q_heads: int, num_kv_heads: int, hea
         num_pages = B * bt_stride
         table = None
     store = np.uint16 if dtype == BF16 else np.float32
+    if not fill:
+        def shaped(shape):
+            return np.broadcast_to(np.zeros((), store), shape)
+        return Case(name, dtype, hq, hkv, d, P, L, n, cu, shaped((T, hq, d)), shaped((T, hkv, d)),
+                    shaped((T, hkv, d)), shaped((num_pages, P, hkv, d)), shaped((num_pages, P, hkv, d)), table,
+                    bt_stride, seed)
     canary = CANARY_BF16 if dtype == BF16 else CANARY_F32.view(np.float32)
     k_pool = np.full((num_pages, P, hkv, d), canary, dtype=store)
     v_pool = np.full((num_pages, P, hkv, d), canary, dtype=store)
