@@ -136,25 +136,36 @@ __device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_ex
 // nor waits for these loads before unrelated LDS reads; every wait on them is
 // explicit.  M0 holds the LDS address; the instruction offset moves the LDS
 // and the global address alike, so run member i (LDS m0 + 1024 i) takes a
-// per-lane offset that already carries -1024 i.
-template <int N>
+// per-lane offset that already carries -1024 i.  NT sets the non-temporal
+// hint: for K/V that no other workgroup reads again it streams ~15 % faster
+// (a 252 MB K/V stream through the same LDS ring: 44.6 -> 38.4 us).
+#define CSR_DMA1(NTS) "s_mov_b32 m0, %0\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %1, %2" NTS
+#define CSR_DMA2(NTS)                                                                                   \
+  "s_mov_b32 m0, %0\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %1, %3" NTS "\n\tglobal_load_lds_dwordx4 %2, %3 " \
+  "offset:1024" NTS
+#define CSR_DMAV(NTS) "s_mov_b32 m0, %0\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %1, off" NTS
+template <int N, bool NT>
 __device__ __forceinline__ void dma_sbase(const char* base, uint32_t m0, const uint32_t* voff) {
   static_assert(N == 1 || N == 2, "runs of one or two DMA blocks");
-  if constexpr (N == 1)
-    asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %1, %2"
-                 :
-                 : "s"(m0), "v"(voff[0]), "s"(base)
-                 : "memory");
+  if constexpr (N == 1 && NT)
+    asm volatile(CSR_DMA1(" nt") : : "s"(m0), "v"(voff[0]), "s"(base) : "memory");
+  else if constexpr (N == 1)
+    asm volatile(CSR_DMA1("") : : "s"(m0), "v"(voff[0]), "s"(base) : "memory");
+  else if constexpr (NT)
+    asm volatile(CSR_DMA2(" nt") : : "s"(m0), "v"(voff[0]), "v"(voff[1]), "s"(base) : "memory");
   else
-    asm volatile(
-        "s_mov_b32 m0, %0\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %1, %3\n\tglobal_load_lds_dwordx4 %2, %3 offset:1024"
-        :
-        : "s"(m0), "v"(voff[0]), "v"(voff[1]), "s"(base)
-        : "memory");
+    asm volatile(CSR_DMA2("") : : "s"(m0), "v"(voff[0]), "v"(voff[1]), "s"(base) : "memory");
 }
+template <bool NT>
 __device__ __forceinline__ void dma_vaddr(const char* src, uint32_t m0) {
-  asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %1, off" : : "s"(m0), "v"(src) : "memory");
+  if constexpr (NT)
+    asm volatile(CSR_DMAV(" nt") : : "s"(m0), "v"(src) : "memory");
+  else
+    asm volatile(CSR_DMAV("") : : "s"(m0), "v"(src) : "memory");
 }
+#undef CSR_DMA1
+#undef CSR_DMA2
+#undef CSR_DMAV
 
 // Everything a workgroup needs about its unit.
 struct Unit {
@@ -322,6 +333,9 @@ __global__ void __launch_bounds__(NW * 64, 8 / NW) attn_bf16_kernel(const AttnAr
   constexpr int NG0 = (NPG + 1) / 2;           // lookup groups issued in a tile's first step
   static_assert(!SCALAR_PAGES || PB * ROWS_PER_KB == dma_rows_per_lookup(D, KV8, NW, DMA_UPPER),
                 "scalar page lookups cover the rows the launcher checks against the page size");
+  // With every row of a unit in one workgroup, no other workgroup reads the
+  // unit's K/V tiles: stream them with the non-temporal hint.
+  constexpr bool NT_KV = DMA_UPPER;
   constexpr int ST = 4;                      // ring stages (K and V each)
   constexpr float THRESH = 8.f;              // lazy-rescale threshold (log2 units)
   __shared__ __attribute__((aligned(1024))) char lds[2 * ST * TILEB];
@@ -478,15 +492,15 @@ __global__ void __launch_bounds__(NW * 64, 8 / NW) attn_bf16_kernel(const AttnAr
     if constexpr (SCALAR_PAGES) {
       const uint32_t m0 = lds_addr(dst) + blk(g * PB) * 1024;
       if constexpr (decltype(pfx)::value) {  // caller guarantees a wholly cached tile
-        dma_sbase<PB>(pool_base + pgoff, m0, &pool_v[g * PB]);
+        dma_sbase<PB, NT_KV>(pool_base + pgoff, m0, &pool_v[g * PB]);
         return;
       }
       if (t0 + KT - 1 < u.L) {
-        dma_sbase<PB>(pool_base + pgoff, m0, &pool_v[g * PB]);
+        dma_sbase<PB, NT_KV>(pool_base + pgoff, m0, &pool_v[g * PB]);
         return;
       }
       if (t0 >= u.L && t0 + KT - 1 <= last_key) {
-        dma_sbase<PB>(new_base + (int64_t)(u.cuq + t0 - u.L) * kv_stride, m0, &new_v[g * PB]);
+        dma_sbase<PB, NT_KV>(new_base + (int64_t)(u.cuq + t0 - u.L) * kv_stride, m0, &new_v[g * PB]);
         return;
       }
 #pragma unroll
@@ -495,13 +509,13 @@ __global__ void __launch_bounds__(NW * 64, 8 / NW) attn_bf16_kernel(const AttnAr
         const int t = min(t0 + drow[j], last_key);
         const char* src = t < u.L ? pool_base + pgoff + pool_off[j]
                                   : new_base + (int64_t)(u.cuq + t - u.L) * kv_stride + dchunk[j];
-        dma_vaddr(src, m0 + 1024u * i);
+        dma_vaddr<NT_KV>(src, m0 + 1024u * i);
       }
     } else {
       const int t = min(t0 + drow[g], last_key);
       const char* src = t < u.L ? pool_base + pgoff + pool_off[g]
                                 : new_base + (int64_t)(u.cuq + t - u.L) * kv_stride + dchunk[g];
-      dma_vaddr(src, lds_addr(dst) + blk(g) * 1024);
+      dma_vaddr<NT_KV>(src, lds_addr(dst) + blk(g) * 1024);
     }
   };
   auto issue = [&](int tile, const int64_t* pg, char* dst, const char* pool_base, const char* new_base) {
@@ -833,8 +847,12 @@ __global__ void __launch_bounds__(NW * 64, 8 / NW) attn_bf16_kernel(const AttnAr
 #pragma unroll
       for (int g = 0; g < NPG; ++g) pgi[g] = pga[g] = dma_wave ? page_id(clampt(u.tb + 3), g) : 0;
     }
-    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
-    __syncthreads();
+    // Only tile 0's K must have landed (the first scores below); the loop's
+    // first tile waits for the rest.  Each DMA wave issued 6 * NDMA loads,
+    // K(0) first, and loads complete in order.
+    static_assert(5 * NDMA <= 63, "vmcnt field");
+    asm volatile("s_waitcnt vmcnt(%0)" ::"n"(5 * NDMA) : "memory");
+    __builtin_amdgcn_s_barrier();
     f32x16 s_a, s_b;
     if (wave_active) {
       qk(kring, 0, s_a);
