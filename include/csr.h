@@ -280,8 +280,8 @@ csr_status csr_set_attention_events(void* begin_event, void* end_event);
  */
 csr_status csr_set_plan_overrides(int32_t nsplit, int32_t fixed_order, int32_t dma_all_waves);
 
-/* Static name of a status code. */
-const char* csr_status_string(csr_status status);
+/* Static name of a status code (any int: values outside csr_status give "CSR_E_UNKNOWN"). */
+const char* csr_status_string(int32_t status);
 
 /* Thread-local description of the last failure on this thread ("" if none). */
 const char* csr_last_error(void);

@@ -13,7 +13,9 @@ import numpy as np
 
 HERE = os.path.dirname(os.path.abspath(__file__))
 SRC = os.path.join(HERE, "csr_oracle.c")
-LIB = os.path.join(HERE, "liboracle.so")
+# CSR_ORACLE_LIBRARY: a separately built copy of the same source (e.g. with
+# host sanitizers); default: the in-tree build.
+LIB = os.environ.get("CSR_ORACLE_LIBRARY") or os.path.join(HERE, "liboracle.so")
 
 F32, BF16 = 0, 1
 ROPE_NONE, ROPE_NEOX, ROPE_INTERLEAVED = 0, 1, 2
@@ -32,7 +34,8 @@ def build() -> str:
 def _load():
     global _lib
     if _lib is None:
-        if not os.path.exists(LIB) or os.path.getmtime(LIB) < os.path.getmtime(SRC):
+        if not os.environ.get("CSR_ORACLE_LIBRARY") and (
+                not os.path.exists(LIB) or os.path.getmtime(LIB) < os.path.getmtime(SRC)):
             build()
         lib = ctypes.CDLL(LIB)
         p, i, d = ctypes.c_void_p, ctypes.c_int, ctypes.c_double

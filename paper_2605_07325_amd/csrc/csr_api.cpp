@@ -441,7 +441,7 @@ csr_status scratch_of_current_device(void** out) {
 
 extern "C" {
 
-const char* csr_status_string(csr_status s) {
+const char* csr_status_string(int32_t s) {
   switch (s) {
     case CSR_OK: return "CSR_OK";
     case CSR_E_INVAL: return "CSR_E_INVAL";
