@@ -313,7 +313,10 @@ def run_asr(args, torch, csr):
 
     def run(mode, limit=None):
         if mode == "asr":
-            ps, ss = torch.cuda.Stream(), asr.cu_masked_stream(sec_cus)
+            # the primary may use every CU; it is still a stream of its own queue (a
+            # mask of all CUs): a stream from torch's pool shared a hardware queue with
+            # the secondary after some sequences of earlier runs, and then waited for it
+            ps, ss = asr.cu_masked_stream(list(range(256))), asr.cu_masked_stream(sec_cus)
         elif mode == "asr_partitioned":
             ps, ss = asr.cu_masked_stream(prim_cus), asr.cu_masked_stream(sec_cus)
         else:
