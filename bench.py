@@ -63,8 +63,15 @@ def log(msg):
 
 
 def kernel_source_hash() -> str:
-    with open(KERNEL_SRC, "rb") as f:
-        return hashlib.sha256(f.read()).hexdigest()[:16]
+    """Hash of extend_attn.hip's code: line comments, trailing blanks and empty
+    lines removed, so that editing a comment does not void the traffic counters."""
+    code = []
+    with open(KERNEL_SRC, encoding="utf-8") as f:
+        for line in f:
+            line = line.split("//", 1)[0].rstrip()
+            if line:
+                code.append(line)
+    return hashlib.sha256("\n".join(code).encode()).hexdigest()[:16]
 
 
 def measured_traffic(workload: str):

@@ -289,14 +289,18 @@ struct TileLoader {
 //
 // Main loop (tiles no row of the workgroup needs masked), software-pipelined
 // per 32-key block b inside every wave: the exponentials of block b are
-// computed while the MFMA pipe works on the scores of block b+1, then P(b) V(b)
-// runs while the row maxima of b+1 are reduced.  The loop is unrolled over the
-// ring so every LDS address is a per-lane register plus an immediate.  The
-// diagonal tiles run afterwards, unpipelined, with the causal mask.
+// computed while the MFMA pipe works on the scores of block b+1, then the
+// block's overflow check and P(b) V(b).  The loop is unrolled over the ring so
+// every LDS address is a per-lane register plus an immediate.  The diagonal
+// tiles run afterwards, unpipelined, with the causal mask.
 //
-// Online softmax keeps a per-row reference max and rescales O only when a new
-// score exceeds it by more than 2^8 (wave-uniform branch); probabilities stay
-// below 2^8 and the final normalisation is exact whatever reference was used.
+// Online softmax keeps a per-row reference max.  In the main loop the
+// probabilities are formed against it and summed per 16-key half-block; a row
+// whose sum passes 2^16 (or is NaN) takes a divergent branch that forms the
+// exact row max, moves the reference and rescales O and the row sum.  The first
+// tile and the diagonal tiles move the reference when a score exceeds it by
+// more than 2^8 (wave-uniform test).  Either way every probability stays below
+// 2^16 and the final normalisation is exact whatever reference was used.
 // NW waves per workgroup, 2 waves per SIMD either way: 8 (one workgroup per
 // CU) or, for an fp8 cache whose 64 KB of rings let two workgroups share a
 // CU, 4 -- decode steps then run two computing waves per CU instead of one.
@@ -337,7 +341,7 @@ __global__ void __launch_bounds__(NW * 64, 8 / NW) attn_bf16_kernel(const AttnAr
   // unit's K/V tiles: stream them with the non-temporal hint.
   constexpr bool NT_KV = DMA_UPPER;
   constexpr int ST = 4;                      // ring stages (K and V each)
-  constexpr float THRESH = 8.f;              // lazy-rescale threshold (log2 units)
+  constexpr float THRESH = 8.f;              // first / diagonal tiles: reference moves past +2^8 (log2 units)
   __shared__ __attribute__((aligned(1024))) char lds[2 * ST * TILEB];
 
   Unit u;
