@@ -24,10 +24,12 @@
 // the token's rows: a neox piece rotates elements [e, e+8) against
 // [e + r/2, e + r/2 + 8), an interleaved piece rotates the four pairs inside
 // [e, e+8), tail pieces (dims >= r) and value rows are copied bit for bit.
-// The rotation itself is fp64 (x cos - x' sin, each product rounded, no fused
-// multiply-add) and each result is rounded once to the element type: bf16
-// directly from fp64, nearest even; fp32 by the plain conversion; an fp8 code
-// from the fp32 value.  The rotated values therefore depend on the inputs and
+// The result is the fp64 rotation (x cos - x' sin, each product rounded, no
+// fused multiply-add) rounded once to the element type: fp32 by the plain
+// conversion; an fp8 code from the fp32 value; bf16 nearest even.  For bf16
+// results an fp32 rotation is used wherever it provably rounds to the same
+// bf16 (almost every element), and the fp64 rotation, rounded to odd in fp32,
+// elsewhere.  The rotated values therefore depend on the inputs and
 // on how closely cos and sin are evaluated, not on any fp32 intermediate.
 // Loads and stores are 16 bytes per lane, and consecutive lanes take
 // consecutive pieces of a row.
@@ -83,31 +85,87 @@ __device__ __forceinline__ void load8(const void* base, int64_t e, float (&x)[8]
   }
 }
 
-// bf16 bit pattern of the nearest bf16 value to v (ties to even), rounded
-// once, directly from fp64.  Normal range: round the fp64 bit pattern at the
-// 8th significant bit (bit 45 of the fraction); below 2^-126, where bf16 steps
-// are 2^-133, scale by 2^133 (exact), round to an integer and scale back.
-__device__ __forceinline__ uint32_t bf16_bits_of(double v) {
-  if (v != v) return 0x7fc0u;
-  const double a = fabs(v);
-  const uint32_t sign = v < 0.0 ? 0x8000u : 0u;
-  if (a < 0x1p-126) {
-    const double q = rint(a * 0x1p133) * 0x1p-133;  // exact in fp32
-    return sign | (__float_as_uint((float)q) >> 16);
+// fp32 value of v rounded to odd: toward zero, with the lowest bit set when
+// inexact.  fp32 keeps 16 more bits than bf16 in the normal and the subnormal
+// range, so rounding this value to bf16 (nearest, ties to even) rounds v
+// itself once.  From 2^-126 up (and for zeros, infinities and NaNs) the low
+// 29 fraction bits of the fp64 pattern are folded into one sticky bit at the
+// fp32 unit, after which the conversion to fp32 is exact (or overflows to
+// infinity, as v's own rounding to bf16 does); below 2^-126 fp32 steps are
+// coarser and a compare against the nearest-even conversion decides.
+__device__ __forceinline__ float f32_round_odd(double v) {
+  const uint64_t b = (uint64_t)__double_as_longlong(v);
+  const uint32_t hi = (uint32_t)(b >> 32);
+  uint32_t lo = (uint32_t)b;
+  if (((hi >> 20) & 0x7FFu) >= 897u || (b << 1) == 0) {
+    lo = (lo & 0xE0000000u) | ((lo & 0x1FFFFFFFu) != 0u ? 0x20000000u : 0u);
+    return (float)__longlong_as_double((long long)(((uint64_t)hi << 32) | lo));
   }
-  uint64_t b = (uint64_t)__double_as_longlong(a);
-  b += 0xFFFFFFFFFFFull + ((b >> 45) & 1ull);  // ties to even at bit 45
-  b &= ~0x1FFFFFFFFFFFull;
-  const double r = __longlong_as_double((long long)b);
-  if (r > 0x1.FEp127) return sign | 0x7f80u;  // beyond the largest bf16: infinity
-  return sign | (__float_as_uint((float)r) >> 16);  // exact: r is a bf16 value
+  const float t = (float)v;  // nearest even
+  const double back = (double)t;
+  uint32_t tb = __float_as_uint(t);
+  if (back != v) {
+    if (fabs(back) > fabs(v)) tb -= 1;  // rounded away from zero: one step back
+    tb |= 1u;
+  }
+  return __uint_as_float(tb);
+}
+
+// bf16 bit patterns of the nearest bf16 values to v0, v1 (ties to even),
+// rounded once from fp64; a NaN gives the quiet NaN 0x7fc0.
+__device__ __forceinline__ uint32_t bf16x2_bits_of(double v0, double v1) {
+  uint32_t w = pack_bf16x2(f32_round_odd(v0), f32_round_odd(v1));
+  if ((w & 0x7fffu) > 0x7f80u) w = (w & 0xffff0000u) | 0x7fc0u;
+  if ((w & 0x7fff0000u) > 0x7f800000u) w = (w & 0x0000ffffu) | 0x7fc00000u;
+  return w;
+}
+
+// The fp32 rotation of a bf16 pair decides the bf16 result when it lies far
+// enough from every bf16 rounding midpoint.  With c32 = fp32(c), s32 = fp32(s),
+// y = fma(u0, c32, -fp32(u1 s32)) differs from the fp64 rotation
+// fl(fl(u0 c) - fl(u1 s)) by at most 2^-22 (|u0| + |u1|) (three fp32
+// roundings of terms bounded by |u0| + |u1|, plus the fp64 ones); in fp32
+// units of y that is at most 4 m / |y|, m = |u0| + |u1|.  All bf16 midpoints
+// of y's binade sit where the low 16 bits of y are 0x8000 (the nearest ones
+// outside it are 2^14 units away), so a normal, finite y whose low half is
+// more than that bound (with margins for this test's own roundings) from
+// 0x8000 rounds to the same bf16 as the fp64 value.
+__device__ __forceinline__ bool bf16_decided(float y, float m) {
+#pragma clang fp contract(off)
+  const uint32_t bits = __float_as_uint(y) & 0x7fffffffu;
+  const uint32_t ex = bits >> 23;                  // biased exponent: 1 .. 254 for normal, finite y
+  const uint32_t low = bits & 0xffffu;
+  const uint32_t dist = low > 0x8000u ? low - 0x8000u : 0x8000u - low;
+  // the bound in fp32 units of y: 2^-22 m / 2^(e - 23) = m 2^(1 - e), e = ex - 127
+  const float bound = __builtin_ldexpf(m, 128 - (int)ex);
+  // bitwise, not short-circuit: no branches on the common path
+  return (ex - 1u < 254u) & ((float)dist > bound * 1.01f + 2.f) & (bound < 8000.f);
+}
+
+// Rotated bf16 pair (u0 c - u1 s, u1 c + u0 s) as fp32 values whose nearest-even
+// bf16 is the fp64 rotation rounded once: the fp32 rotation where it decides
+// the result, else the fp64 rotation rounded to odd.
+__device__ __forceinline__ void rotate_bf16_pair(float u0, float u1, f32x2 t32, f64x2 t64, float& ya, float& yb) {
+#pragma clang fp contract(off)
+  const float q1 = u1 * t32[1], q0 = u0 * t32[1];
+  ya = fmaf(u0, t32[0], -q1);
+  yb = fmaf(u1, t32[0], q0);
+  const float m = fabsf(u0) + fabsf(u1);
+  if (!(bf16_decided(ya, m) & bf16_decided(yb, m))) {
+    const double d0 = u0, d1 = u1;
+    ya = f32_round_odd(d0 * t64[0] - d1 * t64[1]);
+    yb = f32_round_odd(d1 * t64[0] + d0 * t64[1]);
+    // NaNs as the quiet NaN whose bf16 is 0x7fc0
+    if (ya != ya) ya = __uint_as_float(0x7fc00000u);
+    if (yb != yb) yb = __uint_as_float(0x7fc00000u);
+  }
 }
 
 template <bool BF16>
 __device__ __forceinline__ void store8d(void* base, int64_t e, const double (&y)[8]) {
   if constexpr (BF16) {
-    const u32x4 w = {bf16_bits_of(y[0]) | (bf16_bits_of(y[1]) << 16), bf16_bits_of(y[2]) | (bf16_bits_of(y[3]) << 16),
-                     bf16_bits_of(y[4]) | (bf16_bits_of(y[5]) << 16), bf16_bits_of(y[6]) | (bf16_bits_of(y[7]) << 16)};
+    const u32x4 w = {bf16x2_bits_of(y[0], y[1]), bf16x2_bits_of(y[2], y[3]), bf16x2_bits_of(y[4], y[5]),
+                     bf16x2_bits_of(y[6], y[7])};
     *reinterpret_cast<u32x4*>(static_cast<uint16_t*>(base) + e) = w;
   } else {
     f32x4* p = reinterpret_cast<f32x4*>(static_cast<float*>(base) + e);
@@ -169,7 +227,8 @@ __device__ __forceinline__ void copy8(void* dst, const void* src, int64_t de, in
 }
 
 template <bool BF16, bool KV8>
-__device__ __forceinline__ void rotate_piece(const RopeArgs& a, const f64x2* cs, int tok, int64_t slot, int u,
+__device__ __forceinline__ void rotate_piece(const RopeArgs& a, const f64x2* cs, const f32x2* cs32, int tok,
+                                             int64_t slot, int u,
                                              int rot_units, int per_row, int n_rot, int nq, bool neox) {
 #pragma clang fp contract(off)
   const int d = a.d;
@@ -228,6 +287,20 @@ __device__ __forceinline__ void rotate_piece(const RopeArgs& a, const f64x2* cs,
     double y0[8], y1[8];
     load8<BF16>(src, row + e0, x0);
     load8<BF16>(src, row + e1, x1);
+    if (BF16 && !quant) {  // bf16 results: fp32 rotation, fp64 where it does not decide the rounding
+      float z0[8], z1[8];
+#pragma unroll
+      for (int j = 0; j < 8; ++j) rotate_bf16_pair(x0[j], x1[j], cs32[e0 + j], cs[e0 + j], z0[j], z1[j]);
+      if (out) {
+        store8<true>(out, row + e0, z0);
+        store8<true>(out, row + e1, z1);
+      }
+      if (pool) {
+        store8<true>(pool, prow + e0, z0);
+        store8<true>(pool, prow + e1, z1);
+      }
+      return;
+    }
 #pragma unroll
     for (int j = 0; j < 8; ++j) {
       const f64x2 t = cs[e0 + j];
@@ -248,6 +321,15 @@ __device__ __forceinline__ void rotate_piece(const RopeArgs& a, const f64x2* cs,
     float x[8];
     double y[8];
     load8<BF16>(src, row + e0, x);
+    if (BF16 && !quant) {
+      float z[8];
+#pragma unroll
+      for (int j = 0; j < 4; ++j)
+        rotate_bf16_pair(x[2 * j], x[2 * j + 1], cs32[(e0 >> 1) + j], cs[(e0 >> 1) + j], z[2 * j], z[2 * j + 1]);
+      if (out) store8<true>(out, row + e0, z);
+      if (pool) store8<true>(pool, prow + e0, z);
+      return;
+    }
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
       const f64x2 t = cs[(e0 >> 1) + j];
@@ -263,6 +345,7 @@ __device__ __forceinline__ void rotate_piece(const RopeArgs& a, const f64x2* cs,
 template <bool BF16, bool KV8>
 __global__ void __launch_bounds__(256) rope_append_kernel(RopeArgs a) {
   __shared__ f64x2 cs[64];
+  __shared__ f32x2 cs32[64];
   const int tok = blockIdx.x;
   const int b = token_sequence(a.cu_q, a.batch, tok);
   const int64_t pos = (int64_t)(a.cache_len ? a.cache_len[b] : 0) + (tok - a.cu_q[b]);
@@ -272,6 +355,7 @@ __global__ void __launch_bounds__(256) rope_append_kernel(RopeArgs a) {
     double s, c;
     sincos(angle, &s, &c);
     cs[threadIdx.x] = f64x2{c, s};
+    cs32[threadIdx.x] = f32x2{(float)c, (float)s};
   }
 
   // Cache slot of this token (pool writes only); an invalid page drops them.
@@ -294,7 +378,7 @@ __global__ void __launch_bounds__(256) rope_append_kernel(RopeArgs a) {
   const int v_units = (slot >= 0 || (KV8 && a.v_out)) ? a.Hkv * (d >> 3) : 0;
 
   for (int u = blockIdx.y * blockDim.x + threadIdx.x; u < rot_units + v_units; u += gridDim.y * blockDim.x)
-    rotate_piece<BF16, KV8>(a, cs, tok, slot, u, rot_units, per_row, n_rot, nq, neox);
+    rotate_piece<BF16, KV8>(a, cs, cs32, tok, slot, u, rot_units, per_row, n_rot, nq, neox);
 }
 
 }  // namespace

@@ -101,6 +101,32 @@ def test_rope_kv_append_alone(label, style, r, theta, kw):
     check_rope_pool(case, dev, (style, r, theta), case.cache_len)
 
 
+@pytest.mark.parametrize("where", ["subnormal", "overflow", "nan_inf"])
+def test_rope_append_rounding_at_the_range_ends(where):
+    """Keys in bf16's subnormal range (N(0,1) x 2^-128), and keys of magnitude 2.5e38 - 3.3e38
+    with random signs, whose rotations pass bf16's largest value at most angles (those round to
+    infinity): the single rounding from fp64 holds there too."""
+    case = dg.make_case("rope_range", dtype=dg.BF16, num_q_heads=8, num_kv_heads=2, head_dim=128,
+                        cache_len=[40], seqlen_q=[300], page_size=16, seed=4, cfg_id=502,
+                        scale=2.0 ** -128 if where == "subnormal" else 1.0 if where == "overflow" else 0.5)
+    if where == "overflow":
+        g = dg.rng(4, 502, 7)
+        mag = g.uniform(2.5e38, 3.3e38, size=case.k_new.shape).astype(np.float32)
+        case.k_new = dg.to_bf16_bits(np.where(g.integers(0, 2, size=mag.shape) == 1, mag, -mag))
+    elif where == "nan_inf":  # a sprinkling of NaNs (two payloads) and infinities: NaN results are 0x7fc0
+        g = dg.rng(4, 502, 8)
+        k = case.k_new.copy()
+        special = np.array([0x7fc0, 0xffc1, 0x7f80, 0xff80], dtype=np.uint16)
+        hit = g.random(k.shape) < 0.01
+        k[hit] = special[g.integers(0, 4, size=int(hit.sum()))]
+        case.k_new = k
+    note(f"rope bf16 keys, {where}: csr_kv_append")
+    dev = rope_dev(case, NEOX, 0, 1e4)
+    dev.append()
+    torch.cuda.synchronize()
+    check_rope_pool(case, dev, (NEOX, 0, 1e4), case.cache_len)
+
+
 @pytest.mark.parametrize("n", [512, 1])
 def test_rope_c3_120k_positions(n):
     """Positions 122880 .. 122880 + n - 1: the angle reduction in fp64 keeps the
