@@ -131,6 +131,22 @@ def measured_mfma_peak(torch):
     return fl.value / 1e12, ghz.value, ms.value
 
 
+def measured_hbm_read(torch, nbytes: int):
+    """HBM read ceiling measured on this device (benchmark-support library):
+    GB/s of one launch streaming nbytes with non-temporal loads, back to back,
+    over three rotated copies, and its time per launch in ms."""
+    path = os.path.join(os.path.dirname(os.path.abspath(__file__)), "paper_2605_07325_amd", "libcsr_bench.so")
+    fn = ctypes.CDLL(path).csr_bench_hbm_read
+    fn.restype = ctypes.c_int
+    fn.argtypes = [ctypes.c_size_t, ctypes.c_int, ctypes.c_int, ctypes.c_int] + [ctypes.POINTER(ctypes.c_double)] * 2
+    wgs = torch.cuda.get_device_properties(0).multi_processor_count
+    ms, gbs = ctypes.c_double(), ctypes.c_double()
+    rc = fn((int(nbytes) // 16) * 16, 3, 30, wgs, ctypes.byref(ms), ctypes.byref(gbs))
+    if rc != 0:
+        raise RuntimeError(f"csr_bench_hbm_read failed (HIP error {rc})")
+    return gbs.value, ms.value
+
+
 def cpu_baseline(case, target_s: float):
     """The fp64 oracle timed on this host's cores on a bounded sample of the
     same workload's query tokens (all heads of each sampled token)."""
@@ -258,11 +274,21 @@ def run_sweep(args, torch, csr, dg, names):
         }
         if hbm:
             ent["step_gbs"] = round(abytes / (step_ms * 1e-3) / 1e9, 1)
+            # the same bytes streamed by a plain read kernel on this device, one launch each
+            kv = int(np.sum(2 * case.num_kv_heads * case.head_dim * (1 if fp8 else 2)
+                            * case.cache_len.astype(np.int64)))
+            mg, mms = measured_hbm_read(torch, kv)
+            ent["measured_hbm_read"] = {"gbs": round(mg, 1), "ms": round(mms, 5), "bytes": kv,
+                                        "frac": round(ach / mg, 4),
+                                        "loop": "16-byte non-temporal loads, one 512-thread workgroup per CU, "
+                                                "three rotated copies, back to back"}
         else:
             ent["tflops_step"] = round(flops / (step_ms * 1e-3) / 1e12, 1)
         out["configs"].append(ent)
         log(f"sweep {name}: kernel {kmed:.4f} ms (min {ent['kernel_ms_min']:.4f}), step {step_ms:.4f} ms, "
-            f"{ach:.1f} {unit} = {100 * ach / peak:.1f}% of {peak:g}")
+            f"{ach:.1f} {unit} = {100 * ach / peak:.1f}% of {peak:g}"
+            + (f"; a plain read of its K/V: {ent['measured_hbm_read']['ms'] * 1e3:.1f} us "
+               f"({ent['measured_hbm_read']['gbs']:.0f} GB/s)" if hbm else ""))
         del q, k_new, v_new, pools, o, lse, ws
         torch.cuda.empty_cache()
     return out

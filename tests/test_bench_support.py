@@ -1,4 +1,4 @@
-"""The benchmark-support library (measured MFMA ceiling quoted by bench.py)."""
+"""The benchmark-support library (measured MFMA and HBM-read ceilings quoted by bench.py)."""
 import ctypes
 import os
 
@@ -39,3 +39,34 @@ def test_measured_ceiling_is_plausible():
     assert 0.5 < ghz.value < 2.6
     # the loop issues one 32x32x16 MFMA per 32 clocks per SIMD at most
     assert tflops <= wgs * 4 * 32768 / 32 * ghz.value * 1e9 / 1e12 * 1.02
+
+
+def _hbm():
+    lib = ctypes.CDLL(LIB)
+    fn = lib.csr_bench_hbm_read
+    fn.restype = ctypes.c_int
+    fn.argtypes = [ctypes.c_size_t, ctypes.c_int, ctypes.c_int, ctypes.c_int] + [ctypes.POINTER(ctypes.c_double)] * 2
+    return fn
+
+
+def test_hbm_read_rejects_bad_arguments_before_any_device_call():
+    fn = _hbm()
+    d = [ctypes.c_double() for _ in range(2)]
+    assert fn(0, 3, 10, 256, *map(ctypes.byref, d)) != 0      # no bytes
+    assert fn(1000, 3, 10, 256, *map(ctypes.byref, d)) != 0   # not a multiple of 16
+    assert fn(1 << 20, 0, 10, 256, *map(ctypes.byref, d)) != 0
+    assert fn(1 << 20, 3, 0, 256, *map(ctypes.byref, d)) != 0
+    assert fn(1 << 20, 3, 10, 0, *map(ctypes.byref, d)) != 0
+
+
+@pytest.mark.gpu
+def test_measured_hbm_read_is_plausible():
+    import torch
+
+    torch.cuda.init()
+    fn = _hbm()
+    ms, gbs = ctypes.c_double(), ctypes.c_double()
+    wgs = torch.cuda.get_device_properties(0).multi_processor_count
+    assert fn(251658240, 3, 20, wgs, ctypes.byref(ms), ctypes.byref(gbs)) == 0
+    print(f"measured HBM read: {gbs.value:.0f} GB/s ({ms.value * 1e3:.1f} us per 252 MB)", flush=True)
+    assert 1000 < gbs.value < 8000   # below the published 8 TB/s
