@@ -274,6 +274,8 @@ def run_sweep(args, torch, csr, dg, names):
         }
         if hbm:
             ent["step_gbs"] = round(abytes / (step_ms * 1e-3) / 1e9, 1)
+            wc = workgroup_clock(torch, csr, step, step_ms)
+            ent["workgroup_clock"] = {k: wc[k] for k in ("workgroups", "kernel_us", "end_median_us", "end_max_us")}
             # the same bytes streamed by a plain read kernel on this device, one launch each
             kv = int(np.sum(2 * case.num_kv_heads * case.head_dim * (1 if fp8 else 2)
                             * case.cache_len.astype(np.int64)))
@@ -292,6 +294,42 @@ def run_sweep(args, torch, csr, dg, names):
         del q, k_new, v_new, pools, o, lse, ws
         torch.cuda.empty_cache()
     return out
+
+
+def workgroup_clock(torch, csr, step, step_ms, warm_ms=40.0):
+    """Per-workgroup start / end of the attention kernel (the library's clock hook)
+    in the last of back-to-back steps, that step's kernel time from the event hook
+    beside it, summarised: when the workgroups end relative to the first start, and
+    each XCD's median end.  The steps before it (about ``warm_ms`` of work) bring
+    the clocks back up after the host-side pause before the pass: the first
+    launches after even a short idle spell run up to ~25 % slower, and the rate
+    recovers over some 20 ms of load."""
+    steps = max(10, int(warm_ms / max(step_ms, 1e-3)) + 1)
+    stamps = torch.zeros((8192, 4), dtype=torch.int64, device="cuda")
+    hip = HipEvents()
+    a, b = hip.create(), hip.create()
+    torch.cuda.synchronize()
+    try:
+        for i in range(steps - 1):
+            step(i)
+        csr.set_workgroup_clock(stamps)
+        csr.set_attention_events(a, b)
+        step(steps - 1)
+    finally:
+        csr.set_workgroup_clock(None)
+        csr.set_attention_events(None, None)
+    torch.cuda.synchronize()
+    kernel_us = hip.elapsed_ms(a, b) * 1e3
+    hip.destroy(a)
+    hip.destroy(b)
+    t = csr.workgroup_clock_table(stamps)
+    end = t["end_us"]
+    xcd = [float(np.median(end[t["xcd"] == x])) for x in sorted(set(t["xcd"].tolist()))]
+    return {"workgroups": int(len(end)), "steps": steps, "kernel_us": round(kernel_us, 1),
+            "start_max_us": round(float(t["start_us"].max()), 2),
+            "end_min_us": round(float(end.min()), 2), "end_median_us": round(float(np.median(end)), 2),
+            "end_max_us": round(float(end.max()), 2), "xcd_end_median_us": [round(x, 1) for x in xcd],
+            "xcd_spread_pct": round(100.0 * (max(xcd) - min(xcd)) / max(xcd), 2)}
 
 
 def hooked_kernel_ms(torch, csr, step, steps):
@@ -692,6 +730,12 @@ def main():
     rec["roofline"]["kernel_ms_median"] = round(float(np.median(attn_ms)), 5)
     rec["roofline"]["kernel_ms_min"] = round(float(np.min(attn_ms)), 5)
     rec["roofline"]["kernel_sha"] = kernel_source_hash()
+    if bf16:
+        # per-workgroup clock of the attention kernel (a separate pass: the hook stores two clock values per workgroup)
+        rec["workgroup_clock"] = workgroup_clock(torch, csr, lambda i: step(args.warmup + i), ms_per_step)
+        log(f"workgroup clock (kernel {rec['workgroup_clock']['kernel_us']:.1f} us by events): ends {rec['workgroup_clock']['end_min_us']:.1f} / {rec['workgroup_clock']['end_median_us']:.1f} / "
+            f"{rec['workgroup_clock']['end_max_us']:.1f} us (min / median / max after the first start); XCD medians "
+            f"{rec['workgroup_clock']['xcd_end_median_us']} ({rec['workgroup_clock']['xcd_spread_pct']:.1f} % spread)")
     log(f"step median {rec['step_ms_stats']['median']:.4f} ms, min {rec['step_ms_stats']['min']:.4f} ms; kernel "
         f"median {rec['roofline']['kernel_ms_median']:.4f} ms, min {rec['roofline']['kernel_ms_min']:.4f} ms")
     if bf16:

@@ -265,6 +265,21 @@ csr_status csr_prefill(const csr_attn_desc* desc, int32_t batch, const void* q, 
 csr_status csr_set_attention_events(void* begin_event, void* end_event);
 
 /*
+ * Profiling hook.  While set, the bf16 / fp8 attention kernel of every later
+ * csr_extend_attention / csr_prefill call made on this thread records, for
+ * each workgroup with id < capacity, four 64-bit words at stamps[4 * id]:
+ * the constant 100 MHz clock (s_memrealtime; the rate HIP reports as
+ * hipDeviceAttributeWallClockRate) when the workgroup started and
+ * when it finished its key tiles, its key tiles (first << 32 | end), and
+ * (sequence << 32 | split << 16 | kv head << 8 | XCD).  Workgroups without a
+ * unit write nothing.  stamps is device memory owned by the caller (8-byte
+ * aligned, 32 * capacity bytes); pass NULL, 0 to switch the hook off.
+ * Results are unchanged.  Returns CSR_E_INVAL for a buffer without a
+ * positive capacity or the reverse, or a misaligned buffer.
+ */
+csr_status csr_set_workgroup_clock(void* stamps, int32_t capacity);
+
+/*
  * Testing and A/B measurement only: steer the launch plan of later
  * csr_extend_attention / csr_prefill calls and workspace queries made on this
  * thread (a workspace query and the call it sizes must see the same values).

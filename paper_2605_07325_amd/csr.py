@@ -26,7 +26,8 @@ CSR_NOALLOC_SCRATCH_BYTES = 64 << 20  # include/csr.h
 
 # Every function include/csr.h declares.
 EXPORTS = ("csr_kv_append", "csr_extend_workspace_size", "csr_extend_attention", "csr_prefill_workspace_size",
-           "csr_extend_attention_noalloc", "csr_prefill", "csr_set_attention_events", "csr_set_plan_overrides",
+           "csr_extend_attention_noalloc", "csr_prefill", "csr_set_attention_events", "csr_set_workgroup_clock",
+           "csr_set_plan_overrides",
            "csr_status_string", "csr_last_error")
 
 
@@ -70,6 +71,8 @@ def lib() -> ctypes.CDLL:
         L.csr_prefill.restype = ctypes.c_int
         L.csr_set_attention_events.argtypes = [p, p]
         L.csr_set_attention_events.restype = ctypes.c_int
+        L.csr_set_workgroup_clock.argtypes = [p, i32]
+        L.csr_set_workgroup_clock.restype = ctypes.c_int
         L.csr_set_plan_overrides.argtypes = [i32, i32, i32]
         L.csr_set_plan_overrides.restype = ctypes.c_int
         L.csr_status_string.argtypes = [ctypes.c_int]
@@ -96,6 +99,31 @@ def set_attention_events(begin_event, end_event) -> None:
     """csr_set_attention_events: raw hipEvent_t handles (ints) or None to disable."""
     _check(lib().csr_set_attention_events(None if begin_event is None else ctypes.c_void_p(begin_event),
                                           None if end_event is None else ctypes.c_void_p(end_event)))
+
+
+def set_workgroup_clock(stamps=None) -> None:
+    """csr_set_workgroup_clock: an int64 device tensor of shape [capacity, 4], or None to disable."""
+    if stamps is None:
+        _check(lib().csr_set_workgroup_clock(None, 0))
+        return
+    if stamps.dtype != torch.int64 or stamps.dim() != 2 or stamps.shape[1] != 4 or not stamps.is_cuda \
+            or not stamps.is_contiguous():
+        raise ValueError("workgroup clock buffer: a contiguous int64 CUDA tensor of shape [capacity, 4]")
+    _check(lib().csr_set_workgroup_clock(_ptr(stamps), int(stamps.shape[0])))
+
+
+def workgroup_clock_table(stamps) -> "dict":
+    """Decode a filled [capacity, 4] buffer (copied to the host) into arrays: start and end in
+    microseconds from the first start, first / end key tile, sequence, split, kv head, XCD."""
+    import numpy as np
+    w = stamps.cpu().numpy().view(np.uint64)
+    used = w[:, 1] > 0
+    w = w[used]
+    t0 = w[:, 0].min() if len(w) else 0
+    return {"start_us": (w[:, 0] - t0).astype(np.float64) * 0.01, "end_us": (w[:, 1] - t0).astype(np.float64) * 0.01,
+            "tb": (w[:, 2] >> np.uint64(32)).astype(np.int64), "te": (w[:, 2] & np.uint64(0xffffffff)).astype(np.int64),
+            "seq": (w[:, 3] >> np.uint64(32)).astype(np.int64), "split": ((w[:, 3] >> np.uint64(16)) & np.uint64(0xffff)).astype(np.int64),
+            "kv_head": ((w[:, 3] >> np.uint64(8)) & np.uint64(0xff)).astype(np.int64), "xcd": (w[:, 3] & np.uint64(0xff)).astype(np.int64)}
 
 
 def set_plan_overrides(nsplit: int = 0, fixed_order: bool = False, dma_all_waves: bool = False) -> None:

@@ -21,6 +21,8 @@ namespace {
 
 thread_local std::string g_last_error;
 thread_local hipEvent_t g_ev_begin = nullptr, g_ev_end = nullptr;  // csr_set_attention_events
+thread_local uint64_t* g_wg_clock = nullptr;                         // csr_set_workgroup_clock
+thread_local int32_t g_wg_clock_cap = 0;
 // csr_set_plan_overrides (testing and A/B measurement): 0 = the planner's choice.
 struct PlanOverrides {
   int nsplit = 0;         // > 0: key-range splits per unit
@@ -369,6 +371,8 @@ csr_status run_attention(const csr_attn_desc* d, int batch, const void* q, const
   a.xcd_remap = p.xcd_remap;
   a.order = nullptr;
   a.order_slots = 0;
+  a.wg_clock = g_wg_clock;
+  a.wg_clock_cap = g_wg_clock_cap;
   if (p.order_slots > 0) {
     csr::PlanArgs pa;
     pa.cu_q = cu;
@@ -459,6 +463,16 @@ csr_status csr_set_attention_events(void* begin_event, void* end_event) {
     return fail(CSR_E_INVAL, "set both events or neither");
   g_ev_begin = static_cast<hipEvent_t>(begin_event);
   g_ev_end = static_cast<hipEvent_t>(end_event);
+  return CSR_OK;
+}
+
+csr_status csr_set_workgroup_clock(void* stamps, int32_t capacity) {
+  if ((stamps == nullptr) != (capacity == 0) || capacity < 0)
+    return fail(CSR_E_INVAL, "workgroup clock: a buffer and a positive capacity, or NULL and 0 (got %p, %d)", stamps,
+                capacity);
+  if (reinterpret_cast<uintptr_t>(stamps) % 8 != 0) return fail(CSR_E_INVAL, "workgroup clock buffer not 8-byte aligned");
+  g_wg_clock = static_cast<uint64_t*>(stamps);
+  g_wg_clock_cap = capacity;
   return CSR_OK;
 }
 

@@ -317,6 +317,10 @@ struct TileLoader {
 // two 16-byte chunks of the key row in LDS, two of the query row.
 template <int D, bool SCALAR_PAGES, bool KV8 = false, int NW = 8, bool DMA_UPPER = false, bool QK8 = false>
 __global__ void __launch_bounds__(NW * 64, 8 / NW) attn_bf16_kernel(const AttnArgs a) {
+  // Profiling hook: the 100 MHz constant clock at the start, stored at once
+  // (nothing stays live for it); the end fields follow in the epilogue.
+  if (a.wg_clock && threadIdx.x == 0 && (int)blockIdx.x < a.wg_clock_cap)
+    a.wg_clock[4 * (size_t)blockIdx.x] = __builtin_amdgcn_s_memrealtime();
   static_assert(!KV8 || D == 128, "fp8 K/V rows are laid out for d = 128");
   static_assert(NW == 8 || (NW == 4 && KV8), "4-wave workgroups only with the 64 KB fp8 rings");
   static_assert(!QK8 || KV8, "fp8 score products need the fp8 cache");
@@ -1021,6 +1025,17 @@ __global__ void __launch_bounds__(NW * 64, 8 / NW) attn_bf16_kernel(const AttnAr
     __syncthreads();
   }
 
+  // Profiling hook: end of this workgroup's key tiles on the 100 MHz
+  // constant clock, the tiles, and its unit and XCD.
+  if (a.wg_clock && threadIdx.x == 0 && (int)blockIdx.x < a.wg_clock_cap) {
+    uint32_t xcc;
+    asm volatile("s_getreg_b32 %0, hwreg(HW_REG_XCC_ID)" : "=s"(xcc));
+    uint64_t* w = a.wg_clock + 4 * (size_t)blockIdx.x;
+    w[1] = __builtin_amdgcn_s_memrealtime();
+    w[2] = ((uint64_t)(uint32_t)u.tb << 32) | (uint32_t)u.te;
+    w[3] = ((uint64_t)(uint32_t)u.b << 32) | ((uint64_t)(u.s & 0xffff) << 16) | ((uint64_t)(u.g & 0xff) << 8) |
+           (xcc & 0xffu);
+  }
   // Epilogue: combine the two half-rows' sums, normalise, write o and lse (or split partials).
   const auto pr = __builtin_amdgcn_permlane32_swap(__float_as_uint(lrow), __float_as_uint(lrow), false, false);
   const float lsum = __uint_as_float(pr[0]) + __uint_as_float(pr[1]);

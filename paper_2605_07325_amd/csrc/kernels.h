@@ -37,6 +37,8 @@ struct AttnArgs {
   int32_t xcd_remap;         // 1: keep units that share K/V on one XCD
   const int32_t* order;      // unit of each workgroup (-1: none), or nullptr for the fixed order
   int32_t order_slots;       // with `order`: the grid is 8 * order_slots workgroups
+  uint64_t* wg_clock;        // profiling: 4 words per workgroup (start, end, key tiles, unit and XCD), or nullptr
+  int32_t wg_clock_cap;      // workgroups that record (workgroup id < cap)
 };
 
 // Packed rows (query token x head-in-group) per workgroup for each kernel.

@@ -146,6 +146,16 @@ def test_event_hook_requires_both_events():
     assert lib.csr_set_attention_events(None, None) == csr.CSR_OK
 
 
+def test_workgroup_clock_hook_validation():
+    lib = csr.lib()
+    assert lib.csr_set_workgroup_clock(None, 5) == csr.CSR_E_INVAL
+    assert lib.csr_set_workgroup_clock(ctypes.c_void_p(FAKE), 0) == csr.CSR_E_INVAL
+    assert lib.csr_set_workgroup_clock(ctypes.c_void_p(FAKE), -1) == csr.CSR_E_INVAL
+    assert lib.csr_set_workgroup_clock(ctypes.c_void_p(FAKE + 4), 8) == csr.CSR_E_INVAL   # misaligned
+    assert lib.csr_set_workgroup_clock(ctypes.c_void_p(FAKE), 8) == csr.CSR_OK
+    assert lib.csr_set_workgroup_clock(None, 0) == csr.CSR_OK
+
+
 @pytest.mark.parametrize("over,code", [
     (dict(rope_style=3, rope_theta=1e4), csr.CSR_E_INVAL),                 # unknown pairing
     (dict(rope_style=csr.CSR_ROPE_NEOX, rope_theta=0.0), csr.CSR_E_INVAL),  # no base
