@@ -53,6 +53,7 @@ sys.path.insert(0, ROOT)
 PEAK_BF16_TFLOPS = 2500.0   # MI355X dense bf16 MFMA (published)
 PEAK_FP8_TFLOPS = 5000.0    # MI355X dense fp8 MFMA (published)
 PEAK_F32_TFLOPS = 157.3     # MI355X fp32 matrix (published)
+MALL_FLUSH_BYTES = 512 << 20  # twice the 256 MB Infinity Cache
 PEAK_HBM_GBS = 8000.0       # MI355X HBM3E (published)
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic_extend_attn.json")
 KERNEL_SRC = os.path.join(ROOT, "paper_2605_07325_amd", "csrc", "extend_attn.hip")
@@ -131,17 +132,17 @@ def measured_mfma_peak(torch):
     return fl.value / 1e12, ghz.value, ms.value
 
 
-def measured_hbm_read(torch, nbytes: int):
+def measured_hbm_read(torch, nbytes: int, copies: int = 3):
     """HBM read ceiling measured on this device (benchmark-support library):
     GB/s of one launch streaming nbytes with non-temporal loads, back to back,
-    over three rotated copies, and its time per launch in ms."""
+    over ``copies`` rotated copies, and its time per launch in ms."""
     path = os.path.join(os.path.dirname(os.path.abspath(__file__)), "paper_2605_07325_amd", "libcsr_bench.so")
     fn = ctypes.CDLL(path).csr_bench_hbm_read
     fn.restype = ctypes.c_int
     fn.argtypes = [ctypes.c_size_t, ctypes.c_int, ctypes.c_int, ctypes.c_int] + [ctypes.POINTER(ctypes.c_double)] * 2
     wgs = torch.cuda.get_device_properties(0).multi_processor_count
     ms, gbs = ctypes.c_double(), ctypes.c_double()
-    rc = fn((int(nbytes) // 16) * 16, 3, 30, wgs, ctypes.byref(ms), ctypes.byref(gbs))
+    rc = fn((int(nbytes) // 16) * 16, int(copies), 30, wgs, ctypes.byref(ms), ctypes.byref(gbs))
     if rc != 0:
         raise RuntimeError(f"csr_bench_hbm_read failed (HIP error {rc})")
     return gbs.value, ms.value
@@ -181,7 +182,7 @@ def cpu_baseline(case, target_s: float):
                        f"({fl / 1e9:.1f} GFLOP, {dt:.1f} s; full layer extrapolates to {full_s:.0f} s)")}
 
 
-SWEEP_DEFAULT = "c3_1,c3_1_fp8,c3_64,c3_128,c3_1024,c2,c5,c4_61440"
+SWEEP_DEFAULT = "c3_1,c3_1_fp8,c3_64,c3_128,c3_1024,c2,c5,c4_61440,tp4_512,tp4_1"
 
 
 def run_sweep(args, torch, csr, dg, names):
@@ -212,7 +213,11 @@ def run_sweep(args, torch, csr, dg, names):
 
         q, k_new, v_new = normal(case.q.shape), normal(case.k_new.shape), normal(case.v_new.shape)
         mk = codes if fp8 else normal
-        pools = [(mk(case.k_pool.shape), mk(case.v_pool.shape)) for _ in range(max(1, args.pools))]
+        # enough rotated copies that no step finds its K/V in the 256 MB Infinity Cache (one kv head's
+        # 63 MB prefix would otherwise stay resident across the steps)
+        pool_bytes = 2 * case.k_pool.size * (1 if fp8 else 2)
+        pools = [(mk(case.k_pool.shape), mk(case.v_pool.shape))
+                 for _ in range(args.pools if args.pools <= 1 else max(args.pools, -(-MALL_FLUSH_BYTES // pool_bytes)))]
         bt = None if case.block_table is None else torch.from_numpy(case.block_table).cuda()
         cu = torch.from_numpy(case.cu_seqlens_q).cuda()
         cl = torch.from_numpy(case.cache_len).cuda()
@@ -279,11 +284,12 @@ def run_sweep(args, torch, csr, dg, names):
             # the same bytes streamed by a plain read kernel on this device, one launch each
             kv = int(np.sum(2 * case.num_kv_heads * case.head_dim * (1 if fp8 else 2)
                             * case.cache_len.astype(np.int64)))
-            mg, mms = measured_hbm_read(torch, kv)
+            copies = max(3, -(-MALL_FLUSH_BYTES // kv))
+            mg, mms = measured_hbm_read(torch, kv, copies)
             ent["measured_hbm_read"] = {"gbs": round(mg, 1), "ms": round(mms, 5), "bytes": kv,
                                         "frac": round(ach / mg, 4),
                                         "loop": "16-byte non-temporal loads, one 512-thread workgroup per CU, "
-                                                "three rotated copies, back to back"}
+                                                f"{copies} rotated copies, back to back"}
         else:
             ent["tflops_step"] = round(flops / (step_ms * 1e-3) / 1e12, 1)
         out["configs"].append(ent)
@@ -581,7 +587,11 @@ def main():
     q, k_new, v_new = dev(case.q), dev(case.k_new), dev(case.v_new)
     pools = [((torch.from_numpy(case.k_pool).cuda(), torch.from_numpy(case.v_pool).cuda()) if fp8
               else (dev(case.k_pool), dev(case.v_pool)))]
-    for _ in range(max(1, args.pools) - 1):
+    # copies rotated across steps: --pools, and at least enough that no step finds its K/V in the
+    # 256 MB Infinity Cache (--pools 1 keeps one copy, for counter runs)
+    pool_bytes = 2 * pools[0][0].numel() * pools[0][0].element_size()
+    ncopies = args.pools if args.pools <= 1 else max(args.pools, -(-MALL_FLUSH_BYTES // pool_bytes))
+    for _ in range(ncopies - 1):
         pools.append((pools[0][0].clone(), pools[0][1].clone()))
     bt = None if case.block_table is None else torch.from_numpy(case.block_table).cuda()
     cu = torch.from_numpy(case.cu_seqlens_q).cuda()

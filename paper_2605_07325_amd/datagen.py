@@ -11,7 +11,9 @@ across tasks and a freshly computed dynamic part of M tokens (Sec. IV-A, prompt
 construction; N up to 120K and M up to 8192 in the latency sweep), plus the
 eviction-time re-prefill of the compacted history (Algorithm 1, warm-up; the
 experiments evict the oldest half at 110K tokens).  Values are i.i.d. normal,
-scaled, then rounded to bf16 with round-to-nearest-even.
+scaled, then rounded to bf16 with round-to-nearest-even.  One more family holds
+one GPU's share of the 120K-prefix workload when its kv heads are split over
+four GPUs (16 query heads on one kv head).
 """
 from __future__ import annotations
 
@@ -253,7 +255,7 @@ def sample_rows(case: Case, count: int, seed: int = 0, cfg_id: int = 0) -> np.nd
     return np.asarray(chosen, dtype=np.int32)
 
 
-# The five workload families (sizes from the paper's sweeps; see module doc).
+# The workload families (sizes from the paper's sweeps; see module doc).
 def config(cfg: str, seed: int = 0, **over) -> Case:
     if cfg == "c1":  # fp32 single layer, contiguous cache
         kw = dict(dtype=F32, num_q_heads=4, num_kv_heads=1, head_dim=64, cache_len=[1024],
@@ -265,6 +267,10 @@ def config(cfg: str, seed: int = 0, **over) -> Case:
         nq = int(cfg.split("_")[1]) if "_" in cfg else 512
         kw = dict(dtype=BF16, num_q_heads=64, num_kv_heads=4, head_dim=128, cache_len=[122880],
                   seqlen_q=[nq], scale=0.5, cfg_id=3)
+    elif cfg.startswith("tp4"):  # one GPU's share of C3 under 4-way head parallelism: 16q / 1kv, chunk n from the name
+        nq = int(cfg.split("_")[1]) if "_" in cfg else 512
+        kw = dict(dtype=BF16, num_q_heads=16, num_kv_heads=1, head_dim=128, cache_len=[122880],
+                  seqlen_q=[nq], scale=0.5, cfg_id=6)
     elif cfg.startswith("c4"):  # re-prefill of the compacted history, L = 0
         S = int(cfg.split("_")[1]) if "_" in cfg else 61440
         kw = dict(dtype=BF16, num_q_heads=64, num_kv_heads=4, head_dim=128, cache_len=[0],

@@ -106,6 +106,24 @@ def test_c3_120k_prefix_sampled_rows(n):
     compare(case, out, lse, rows, ref, ref_lse, f"c3_{n}")
 
 
+@pytest.mark.parametrize("n", [512, 1])
+def test_tp4_share_of_c3_sampled_rows(n):
+    # one GPU's share of C3 under 4-way head parallelism: 16 query heads on one kv head, the same
+    # 120K prefix (the planner splits the single kv head's keys 8 ways at n = 512)
+    case = dg.config(f"tp4_{n}")
+    note(f"tp4 share bf16 16q/1kv L=122880 n={n}: csr_extend_attention(APPEND)")
+    dev = Dev(case)
+    out, lse = dev.extend(append=True)
+    torch.cuda.synchronize()
+    rows = dg.sample_rows(case, 64, cfg_id=6) if n > 1 else np.arange(case.total_q, dtype=np.int32)
+    ref, ref_lse = oracle_rows(case, rows)
+    compare(case, out, lse, rows, ref, ref_lse, f"tp4_{n}")
+    kp, vp = oracle.kv_append(case.k_new, case.v_new, case.k_pool, case.v_pool, case.block_table, case.bt_stride,
+                              case.cu_seqlens_q, case.cache_len, case.num_kv_heads, case.head_dim, case.page_size)
+    np.testing.assert_array_equal(from_dev(case, dev.k_pool), kp)
+    np.testing.assert_array_equal(from_dev(case, dev.v_pool), vp)
+
+
 @pytest.mark.parametrize("S", [61440, 122880])
 def test_c4_reprefill_sampled_rows_and_cache_write(S):
     case = dg.config(f"c4_{S}")
