@@ -302,7 +302,23 @@ def run_sweep(args, torch, csr, dg, names):
     return out
 
 
-def workgroup_clock(torch, csr, step, step_ms, warm_ms=40.0):
+def clock_detail(t) -> dict:
+    """Breakdown of one clock-hooked launch: per kv head, per split (up to 16) and per XCD,
+    the median end after the first start and the median us per key tile of the workgroups."""
+    end, nt = t["end_us"], np.maximum(t["te"] - t["tb"], 1)
+    rate = (end - t["start_us"]) / nt
+
+    def by(key, limit=None):
+        vals = sorted(set(t[key].tolist()))
+        if limit is not None and len(vals) > limit:
+            return None
+        return {str(v): {"n": int((t[key] == v).sum()), "end_median_us": round(float(np.median(end[t[key] == v])), 2),
+                         "us_per_tile_median": round(float(np.median(rate[t[key] == v])), 4)} for v in vals}
+
+    return {"by_kv_head": by("kv_head"), "by_split": by("split", 16), "by_xcd": by("xcd")}
+
+
+def workgroup_clock(torch, csr, step, step_ms, warm_ms=40.0, detail=False):
     """Per-workgroup start / end of the attention kernel (the library's clock hook)
     in the last of back-to-back steps, that step's kernel time from the event hook
     beside it, summarised: when the workgroups end relative to the first start, and
@@ -335,7 +351,8 @@ def workgroup_clock(torch, csr, step, step_ms, warm_ms=40.0):
             "start_max_us": round(float(t["start_us"].max()), 2),
             "end_min_us": round(float(end.min()), 2), "end_median_us": round(float(np.median(end)), 2),
             "end_max_us": round(float(end.max()), 2), "xcd_end_median_us": [round(x, 1) for x in xcd],
-            "xcd_spread_pct": round(100.0 * (max(xcd) - min(xcd)) / max(xcd), 2)}
+            "xcd_spread_pct": round(100.0 * (max(xcd) - min(xcd)) / max(xcd), 2),
+            **({"detail": clock_detail(t)} if detail else {})}
 
 
 def hooked_kernel_ms(torch, csr, step, steps):
@@ -539,6 +556,10 @@ def main():
     ap.add_argument("--sweep", default="auto",
                     help="comma-separated workloads for the compact 'sweep' record ('' to skip; a _fp8 suffix "
                          f"selects the e4m3 cache); 'auto' = {SWEEP_DEFAULT} with the default workload, none otherwise")
+    ap.add_argument("--clock-detail", action="store_true",
+                    help="add the clock pass's per-kv-head / per-split / per-XCD breakdown (workgroup_clock.detail)")
+    ap.add_argument("--pool-offset", type=int, default=0,
+                    help="place every K/V pool copy this many bytes (a multiple of 16, < 4096) past a 4 KB boundary")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="also run a 1 GiB device copy (HBM counter calibration for rocprofv3 --pmc runs)")
     args = ap.parse_args()
@@ -593,6 +614,21 @@ def main():
     ncopies = args.pools if args.pools <= 1 else max(args.pools, -(-MALL_FLUSH_BYTES // pool_bytes))
     for _ in range(ncopies - 1):
         pools.append((pools[0][0].clone(), pools[0][1].clone()))
+    if args.pool_offset:
+        if args.pool_offset % 16 or not 0 < args.pool_offset < 4096:
+            raise SystemExit("--pool-offset: a multiple of 16 in (0, 4096)")
+
+        def placed(t):
+            # the same bytes at pool_offset past a 4 KB boundary (the kernels need 16-byte alignment)
+            nbytes = t.numel() * t.element_size()
+            buf = torch.empty(nbytes + 8192, dtype=torch.uint8, device="cuda")
+            at = (-buf.data_ptr()) % 4096 + args.pool_offset
+            view = buf[at:at + nbytes].view(t.dtype).view(t.shape)
+            view.copy_(t)
+            return view
+
+        pools = [(placed(k), placed(v)) for k, v in pools]
+        torch.cuda.empty_cache()
     bt = None if case.block_table is None else torch.from_numpy(case.block_table).cuda()
     cu = torch.from_numpy(case.cu_seqlens_q).cuda()
     cl = torch.from_numpy(case.cache_len).cuda()
@@ -694,6 +730,7 @@ def main():
             "gflop_per_step": round(flops / 1e9, 2),
             "algorithmic_mb_per_step": round(abytes / 1e6, 2),
             "pool_copies_rotated": len(pools),
+            **({"pool_offset_bytes": args.pool_offset} if args.pool_offset else {}),
         },
         "roofline": {
             "bound": "mfma",
@@ -742,7 +779,8 @@ def main():
     rec["roofline"]["kernel_sha"] = kernel_source_hash()
     if bf16:
         # per-workgroup clock of the attention kernel (a separate pass: the hook stores two clock values per workgroup)
-        rec["workgroup_clock"] = workgroup_clock(torch, csr, lambda i: step(args.warmup + i), ms_per_step)
+        rec["workgroup_clock"] = workgroup_clock(torch, csr, lambda i: step(args.warmup + i), ms_per_step,
+                                                 detail=args.clock_detail)
         log(f"workgroup clock (kernel {rec['workgroup_clock']['kernel_us']:.1f} us by events): ends {rec['workgroup_clock']['end_min_us']:.1f} / {rec['workgroup_clock']['end_median_us']:.1f} / "
             f"{rec['workgroup_clock']['end_max_us']:.1f} us (min / median / max after the first start); XCD medians "
             f"{rec['workgroup_clock']['xcd_end_median_us']} ({rec['workgroup_clock']['xcd_spread_pct']:.1f} % spread)")

@@ -70,3 +70,29 @@ def test_measured_hbm_read_is_plausible():
     assert fn(251658240, 3, 20, wgs, ctypes.byref(ms), ctypes.byref(gbs)) == 0
     print(f"measured HBM read: {gbs.value:.0f} GB/s ({ms.value * 1e3:.1f} us per 252 MB)", flush=True)
     assert 1000 < gbs.value < 8000   # below the published 8 TB/s
+
+
+def test_clock_detail_groups_a_decoded_table():
+    # bench.py's breakdown of one clock-hooked launch, on a hand-made table: two kv heads on two
+    # XCDs, two splits each; head 1 streams its tiles at twice the time per tile
+    import sys
+
+    import numpy as np
+
+    sys.path.insert(0, os.path.dirname(os.path.dirname(os.path.abspath(__file__))))
+    import bench
+
+    t = {"start_us": np.array([0.0, 0.0, 1.0, 1.0]), "end_us": np.array([10.0, 12.0, 21.0, 25.0]),
+         "tb": np.array([0, 10, 0, 10]), "te": np.array([10, 20, 10, 22]),
+         "kv_head": np.array([0, 0, 1, 1]), "split": np.array([0, 1, 0, 1]), "xcd": np.array([0, 0, 1, 1])}
+    d = bench.clock_detail(t)
+    assert d["by_kv_head"]["0"] == {"n": 2, "end_median_us": 11.0, "us_per_tile_median": 1.1}
+    assert d["by_kv_head"]["1"] == {"n": 2, "end_median_us": 23.0, "us_per_tile_median": 2.0}
+    assert d["by_split"]["1"]["end_median_us"] == 18.5
+    assert d["by_xcd"]["1"]["us_per_tile_median"] == 2.0
+    many = dict(t, split=np.arange(4) * 9)
+    assert bench.clock_detail(many)["by_split"] is not None
+    many["split"] = np.arange(4) + 20
+    t20 = {k: np.concatenate([v] * 5) for k, v in many.items()}
+    t20["split"] = np.arange(20)
+    assert bench.clock_detail(t20)["by_split"] is None  # more than 16 splits: left out
