@@ -530,7 +530,8 @@ def main():
     ap.add_argument("--steps", type=int, default=30)
     ap.add_argument("--warmup", type=int, default=10)
     ap.add_argument("--workload", default="c3_512",
-                    help="c3_<n> extend over a 122880 prefix (default n=512), c2, c5, c1, c4_<S> (prefill), "
+                    help="c3_<n> extend over a 122880 prefix (default n=512), tp4_<n> (its 16q/1kv share), c2, c5, c1, "
+                         "c4_<S> (prefill), "
                          "asr (state reconciliation beside a stream of 100-token tasks)")
     ap.add_argument("--pools", type=int, default=3, help="K/V pool copies rotated across steps")
     ap.add_argument("--no-cpu-baseline", action="store_true")
