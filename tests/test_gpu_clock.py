@@ -56,3 +56,37 @@ def test_workgroup_clock_records_every_unit_and_changes_nothing():
     span_us, event_us = t["end_us"].max(), begin.elapsed_time(end) * 1e3
     assert 0.5 * event_us < span_us <= event_us * 1.01 + 1.0, (span_us, event_us)
     note(f"workgroup clock: 256 units, ends {t['end_us'].min():.1f}..{t['end_us'].max():.1f} us after the first start, launch {event_us:.1f} us")
+
+
+def test_workgroup_clock_on_the_fp8_decode_kernel():
+    # the 4-wave kernel (two workgroups per CU) of an e4m3 cache at n = 1: one record per unit of the
+    # plan, every (kv head, split) pair once, tiles that tile each kv head's key range, outputs unchanged
+    case = dg.with_fp8_pools(dg.make_case("clk8", dtype=dg.BF16, num_q_heads=64, num_kv_heads=4, head_dim=128,
+                                          cache_len=[20000], seqlen_q=[1], seed=5, cfg_id=312), cfg_id=312)
+    dev = Dev(case)
+    dev.k_pool = torch.from_numpy(case.k_pool).cuda()
+    dev.v_pool = torch.from_numpy(case.v_pool).cuda()
+    dev.desc.kv_dtype = csr.CSR_KV_FP8_E4M3
+    dev.desc.k_scale, dev.desc.v_scale = 0.0625, 0.0390625
+    note("workgroup clock: fp8 decode L=20000 n=1 with and without the hook")
+    out0, lse0 = dev.extend()
+    stamps = torch.zeros((4096, 4), dtype=torch.int64, device="cuda")
+    csr.set_workgroup_clock(stamps)
+    try:
+        out1, lse1 = dev.extend()
+    finally:
+        csr.set_workgroup_clock(None)
+    torch.cuda.synchronize()
+    assert torch.equal(out0.view(torch.int16), out1.view(torch.int16)) and torch.equal(lse0, lse1)
+    t = csr.workgroup_clock_table(stamps)
+    splits = int(t["split"].max()) + 1
+    assert len(t["end_us"]) == 4 * splits  # one row tile per kv head at n = 1
+    ntiles = -(-(20000 + 1) // 64)
+    for g in range(4):
+        m = t["kv_head"] == g
+        assert sorted(t["split"][m].tolist()) == list(range(splits))
+        order = np.argsort(t["split"][m])
+        tb, te = t["tb"][m][order], t["te"][m][order]
+        assert tb[0] == 0 and te[-1] == ntiles and np.all(tb[1:] == te[:-1])  # contiguous, complete
+    assert np.all(t["end_us"] >= t["start_us"])
+    note(f"workgroup clock fp8 decode: {4 * splits} units, last end {t['end_us'].max():.1f} us after the first start")

@@ -166,6 +166,50 @@ def test_deterministic(cfg):
     assert torch.equal(l1, l2)
 
 
+def _placed(t, offset):
+    """The same bytes as ``t`` at ``offset`` bytes past a 4 KB boundary (a view into a larger buffer)."""
+    nbytes = t.numel() * t.element_size()
+    buf = torch.empty(nbytes + 8192, dtype=torch.uint8, device="cuda")
+    at = (-buf.data_ptr()) % 4096 + offset
+    view = buf[at:at + nbytes].view(t.dtype).view(t.shape)
+    view.copy_(t)
+    return view
+
+
+@pytest.mark.parametrize("kv", ["bf16", "fp8"])
+@pytest.mark.parametrize("n", [1, 40])
+def test_pool_base_address_does_not_change_results(kv, n):
+    # The contract asks only 16-byte alignment of the pools.  Each kv head's piece of a cached token
+    # row sits at a fixed byte offset of the row, so moving the pool's base moves every DMA source
+    # across 256 B and 1 KB boundaries: the output bits must not move with it (decode and a
+    # multi-tile chunk; bf16 and e4m3 caches).
+    case = dg.make_case("align", dtype=dg.BF16, num_q_heads=64, num_kv_heads=4, head_dim=128, cache_len=[5000],
+                        seqlen_q=[n], seed=11, cfg_id=311)
+    if kv == "fp8":
+        case = dg.with_fp8_pools(case, cfg_id=311)
+    note(f"pool base address {kv} n={n}: csr_extend_attention with the pools at 0 / 16 / 272 / 784 B past 4 KB")
+    dev = Dev(case)
+    if kv == "fp8":
+        dev.k_pool = torch.from_numpy(case.k_pool).cuda()
+        dev.v_pool = torch.from_numpy(case.v_pool).cuda()
+        dev.desc.kv_dtype = csr.CSR_KV_FP8_E4M3
+        dev.desc.k_scale, dev.desc.v_scale = 0.0625, 0.0390625
+    k0, v0 = dev.k_pool, dev.v_pool
+    results = []
+    for off in (0, 16, 272, 784):
+        dev.k_pool, dev.v_pool = _placed(k0, off), _placed(v0, off)
+        assert dev.k_pool.data_ptr() % 4096 == off
+        out, lse = dev.extend()
+        torch.cuda.synchronize()
+        results.append((out.view(torch.int16).cpu(), lse.cpu()))
+    for out, lse in results[1:]:
+        assert torch.equal(out, results[0][0]) and torch.equal(lse, results[0][1])
+    rows = np.arange(case.total_q, dtype=np.int32)
+    if kv == "bf16":  # and the common result is the right one
+        ref, ref_lse = oracle_rows(case, rows)
+        compare(case, out.view(torch.bfloat16).cuda(), lse.cuda(), rows, ref, ref_lse, f"align/{kv}/n={n}")
+
+
 def test_ragged_batch_with_empty_chunks():
     case = dg.make_case("empty", dtype=dg.BF16, num_q_heads=16, num_kv_heads=2, head_dim=128,
                         cache_len=[500, 700, 0, 1200, 64], seqlen_q=[33, 0, 20, 0, 7], page_size=16, scale=0.5,
