@@ -16,7 +16,7 @@
 //     the unit index is remapped to give each XCD a contiguous range of units;
 //     units sharing a K/V stream then share that XCD's L2.
 //
-// Per-tile math (one wave = NB blocks of 32 packed rows; 64 keys per tile)
+// Per-tile math (one wave = 32 packed rows; 64 keys per tile)
 //   S^T = K Q^T with v_mfma_f32_32x32x16_bf16: A = K tile from LDS, B = Q^T in
 //   registers.  The accumulator layout gives each lane one packed row (lane
 //   mod 32) and 16 keys, so the softmax row statistics are lane-local except
@@ -30,9 +30,11 @@
 //   Softmax runs in the log2 domain: scores are scaled by scale*log2(e) and
 //   exponentiated with v_exp_f32.
 //
-// LDS: K and V tiles (64 keys x d) double-buffered; 16-byte chunks of each key
-// row are XOR-swizzled by row so both the 16-byte K reads (32 rows, one chunk)
-// and the transposing V reads (4 rows x 32 bytes) spread over the banks.
+// LDS: K and V tiles (64 keys x d) stream through 4-stage rings filled by LDS
+// DMA in the bf16 / fp8 kernel and through double buffers in the fp32 one;
+// 16-byte chunks of each key row are XOR-swizzled by row so both the 16-byte K
+// reads (32 rows, one chunk) and the transposing V reads (4 rows x 32 bytes)
+// spread over the banks.
 //
 // An fp32 instance uses v_mfma_f32_32x32x2f32 with the same layout scheme and
 // never rounds through bf16.
