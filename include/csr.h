@@ -26,9 +26,11 @@
  * never moves again (prefix stability, Theorem 1).  The first r = rope_dim dims
  * form r/2 pairs; pair i turns by pos * rope_theta^(-2i/r); CSR_ROPE_NEOX pairs
  * dim i with dim i + r/2, CSR_ROPE_INTERLEAVED pairs dim 2i with dim 2i + 1;
- * dims >= r pass through.  Rotated values are computed in fp32 (angles reduced
- * in fp64) and rounded to the element type (nearest, ties to even).  Keys that
- * are already in the cache are read as stored.
+ * dims >= r pass through.  Rotated q and k values are the fp64 rotation
+ * (x cos - x' sin with cos and sin of the fp64 angle, each product rounded, no
+ * fused multiply-add) rounded once to the element type (nearest, ties to
+ * even; with an fp8 cache the key's code is taken from that value rounded to
+ * fp32).  Keys that are already in the cache are read as stored.
  *
  * FP8 KV cache (optional, csr_attn_desc.kv_dtype = CSR_KV_FP8_E4M3): the pools
  * hold OCP e4m3 codes (1 byte: sign, 4 exponent bits with bias 7, 3 mantissa
